@@ -1,0 +1,390 @@
+/*
+ * ORACLE -- test infrastructure, not product code.
+ *
+ * A plain, slow CPU reference of the ADPSGD hot path (Jiang and Agrawal,
+ * "Adaptive Periodic Averaging", arXiv 2007.06134), written from the paper in
+ * fp64.  Only the test suite, the smoke check and the bench's CPU-baseline leg
+ * may load it.  It shares no code, header, table or helper with the HIP
+ * library; the two meet only through the seeded inputs (seed, sizes and
+ * hyper-parameters).
+ *
+ * What it computes, in the paper's order (Algorithm 2, Section III-B):
+ *   per step t (the paper's iteration k):
+ *     cnt += 1
+ *     every worker k takes a local momentum-SGD step on its own replica
+ *     if cnt == p:  cnt = 0; average the replicas; S_t = variance of the
+ *                   pre-average replicas (Var[.] of Section II-B, per tensor);
+ *                   broadcast the average; then either sample C2 (t < K_s) or
+ *                   move p by +-1 against the 0.7 / 1.3 thresholds.
+ * The paper trains CNNs; here the per-worker gradient is the noisy quadratic
+ * stand-in g = h*(x - x*) + sigma*z (the mini-batch gradient of eq. (3) replaced
+ * by an exact gradient plus Gaussian noise), with momentum 0.9 (Section IV-A)
+ * and coupled weight decay.
+ *
+ * Readings of points the paper leaves open (each is stated where it is used):
+ *   - RunningAverage is the cumulative arithmetic mean of S/gamma over the
+ *     sampling-phase syncs.
+ *   - The sync test uses Algorithm 2's counter in both period modes; a constant
+ *     period is Algorithm 2 without controller updates.
+ *   - Momentum buffers are not averaged; only the parameters are.
+ *   - p never drops below 1.
+ *   - The variance divides by K (not K-1) and sums over parameters.
+ *
+ * Conventions the paper does not give (noise law and its generator):
+ *   Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), key = (seed low 32 bits,
+ *   seed high 32 bits), counter = (float4 group g = i/4, worker k, step t, tag);
+ *   tag 0 = gradient noise, 1 = curvature h, 2 = optimum x*.  One call gives the
+ *   four values of elements 4g..4g+3.  Uniform U(r) = (r >> 8) * 2^-24; the
+ *   Box-Muller log argument is ((r0 >> 8) + 1) * 2^-24 in (0, 1].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_PI 3.14159265358979323846
+
+/* ---- Philox4x32-10, from its published definition (SC'11, Sec. 5) ---------
+ * Each round multiplies counter words 0 and 2 by two fixed odd constants,
+ * takes the 64-bit products, and mixes:
+ *   out0 = hi(M1*c2) ^ c1 ^ k0,  out1 = lo(M1*c2),
+ *   out2 = hi(M0*c0) ^ c3 ^ k1,  out3 = lo(M0*c0);
+ * the key is bumped by the Weyl constants between rounds. */
+static const uint32_t PH_M0 = 0xD2511F53u, PH_M1 = 0xCD9E8D57u;
+static const uint32_t PH_W0 = 0x9E3779B9u, PH_W1 = 0xBB67AE85u;
+
+void orc_philox4x32_10(const uint32_t ctr_in[4], const uint32_t key_in[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr_in[0], c1 = ctr_in[1], c2 = ctr_in[2], c3 = ctr_in[3];
+    uint32_t k0 = key_in[0], k1 = key_in[1];
+    for (int round = 0; round < 10; ++round) {
+        uint64_t p0 = (uint64_t)PH_M0 * (uint64_t)c0;
+        uint64_t p1 = (uint64_t)PH_M1 * (uint64_t)c2;
+        uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        uint32_t n1 = (uint32_t)p1;
+        uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        uint32_t n3 = (uint32_t)p0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+        k0 += PH_W0;
+        k1 += PH_W1;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+static void philox_seeded(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                          uint32_t out[4])
+{
+    uint32_t ctr[4] = {c0, c1, c2, c3};
+    uint32_t key[2] = {(uint32_t)(seed & 0xFFFFFFFFu), (uint32_t)(seed >> 32)};
+    orc_philox4x32_10(ctr, key, out);
+}
+
+/* Uniform in [0,1) from the top 24 bits. */
+static double unif24(uint32_t r) { return (double)(r >> 8) * (1.0 / 16777216.0); }
+
+/* Box-Muller (1958): two uniforms -> two independent N(0,1). */
+static void box_muller(uint32_t ra, uint32_t rb, double *z0, double *z1)
+{
+    double u1 = ((double)(ra >> 8) + 1.0) * (1.0 / 16777216.0);   /* (0, 1] */
+    double u2 = unif24(rb);                                      /* [0, 1) */
+    double radius = sqrt(-2.0 * log(u1));
+    *z0 = radius * cos(2.0 * ORC_PI * u2);
+    *z1 = radius * sin(2.0 * ORC_PI * u2);
+}
+
+void orc_normals4(uint64_t seed, uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, double z[4])
+{
+    uint32_t r[4];
+    philox_seeded(seed, c0, c1, c2, c3, r);
+    box_muller(r[0], r[1], &z[0], &z[1]);
+    box_muller(r[2], r[3], &z[2], &z[3]);
+}
+
+/* Raw Box-Muller pair of two 32-bit words (exposed for special-case checks). */
+void orc_box_muller(uint32_t ra, uint32_t rb, double z[2])
+{
+    box_muller(ra, rb, &z[0], &z[1]);
+}
+
+/* Generator dumps over consecutive groups g0 .. g0+n-1 with counter words
+ * (g, c1, c2, c3): raw words out[4n] and the matching normals z[4n]. */
+void orc_philox_groups(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3,
+                       int64_t g0, int64_t n, uint32_t *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j)
+        philox_seeded(seed, (uint32_t)(g0 + j), c1, c2, c3, out + 4 * j);
+}
+
+void orc_normals_groups(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3,
+                        int64_t g0, int64_t n, double *z)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j)
+        orc_normals4(seed, (uint32_t)(g0 + j), c1, c2, c3, z + 4 * j);
+}
+
+/* ---- problem description ------------------------------------------------ */
+typedef struct {
+    int32_t K;                 /* workers (the paper's n) */
+    int32_t T;                 /* tensors */
+    int64_t P;                 /* parameters per replica */
+    const int64_t *offsets;    /* [T+1], offsets[0] = 0, offsets[T] = P */
+    uint64_t seed;
+    double sigma, momentum, weight_decay, h_lo, h_hi;
+    int32_t lr_kind;           /* 0 constant, 1 step decay, 2 cosine */
+    int32_t period_mode;       /* 0 constant period, 1 adaptive (Algorithm 2) */
+    double lr0;
+    int64_t total_steps;
+    int64_t k_s;
+    double thr_lo, thr_hi;
+    int32_t p_init;
+    int32_t pad_;
+} orc_problem;
+
+typedef struct {
+    int64_t t;       /* next step index */
+    int64_t cnt;     /* steps since the last sync */
+    int64_t nC2;     /* syncs folded into C2 */
+    double C2;
+    int32_t p;
+    int32_t pad_;
+} orc_state;
+
+typedef struct {
+    int64_t t;       /* step after which the sync happened */
+    int32_t p;       /* period in force for that sync */
+    int32_t pad_;
+    double S;        /* sum over tensors of the per-tensor variance */
+    double C2;       /* C2 after this sync's update */
+    double gamma;    /* learning rate of step t */
+} orc_sync_rec;
+
+/* Learning rate of 0-based step t.  Step decay: x0.1 at floor(N/2) and again
+ * at floor(3N/4) (the paper decays by 10x at 1/2 and 3/4 of training,
+ * Section IV-B); cosine: lr0 * (1 + cos(pi t / N)) / 2. */
+double orc_lr(const orc_problem *pb, int64_t t)
+{
+    double N = (double)pb->total_steps;
+    switch (pb->lr_kind) {
+    case 1: {
+        double g = pb->lr0;
+        if (t >= pb->total_steps / 2) g *= 0.1;
+        if (t >= (3 * pb->total_steps) / 4) g *= 0.1;
+        return g;
+    }
+    case 2:
+        return pb->lr0 * 0.5 * (1.0 + cos(ORC_PI * (double)t / N));
+    default:
+        return pb->lr0;
+    }
+}
+
+/* Curvature and optimum of element i: h = exp(ln lo + u (ln hi - ln lo)),
+ * u uniform (tag 1); x* ~ N(0,1) (tag 2). */
+void orc_problem_data(const orc_problem *pb, const int64_t *idx, int64_t n, double *h, double *xs)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j) {
+        int64_t i = idx ? idx[j] : j;
+        uint32_t g = (uint32_t)(i / 4);
+        int lane = (int)(i % 4);
+        uint32_t r[4];
+        philox_seeded(pb->seed, g, 0, 0, 1, r);
+        double u = unif24(r[lane]);
+        h[j] = exp(log(pb->h_lo) + u * (log(pb->h_hi) - log(pb->h_lo)));
+        double z[4];
+        orc_normals4(pb->seed, g, 0, 0, 2, z);
+        xs[j] = z[lane];
+    }
+}
+
+/* Gradient noise z for worker k, step t, element i. */
+static double noise(const orc_problem *pb, int32_t k, int64_t t, int64_t i)
+{
+    double z[4];
+    orc_normals4(pb->seed, (uint32_t)(i / 4), (uint32_t)k, (uint32_t)t, 0, z);
+    return z[i % 4];
+}
+
+/* One local step t on every worker (Algorithm 2, lines 6-7, with heavy-ball
+ * momentum as in PyTorch SGD: d = g + wd*x; v = mu*v + d; x = x - gamma*v).
+ * x and v are [K][n] over the selected elements idx[0..n) (all if idx NULL). */
+void orc_local_step(const orc_problem *pb, const int64_t *idx, int64_t n, int64_t t,
+                    const double *h, const double *xs, double *x, double *v)
+{
+    double gamma = orc_lr(pb, t);
+    for (int32_t k = 0; k < pb->K; ++k) {
+        double *xk = x + (int64_t)k * n;
+        double *vk = v + (int64_t)k * n;
+#pragma omp parallel
+        {
+            /* one generator call serves the four elements of a group: keep the
+             * last group's normals (same values as noise(), computed once) */
+            int64_t g_memo = -1;
+            double z4[4] = {0, 0, 0, 0};
+#pragma omp for schedule(static)
+            for (int64_t j = 0; j < n; ++j) {
+                int64_t i = idx ? idx[j] : j;
+                if (i / 4 != g_memo) {
+                    g_memo = i / 4;
+                    orc_normals4(pb->seed, (uint32_t)g_memo, (uint32_t)k, (uint32_t)t, 0, z4);
+                }
+                double z = z4[i % 4];
+                double g = h[j] * (xk[j] - xs[j]) + pb->sigma * z;
+                double d = g + pb->weight_decay * xk[j];
+                vk[j] = pb->momentum * vk[j] + d;
+                xk[j] = xk[j] - gamma * vk[j];
+            }
+        }
+    }
+}
+
+/* Element range [jb, je) of tensor tau within the ascending selection idx. */
+static void tensor_range(const orc_problem *pb, const int64_t *idx, int64_t n, int32_t tau,
+                         int64_t *jb, int64_t *je)
+{
+    if (!idx) { *jb = pb->offsets[tau]; *je = pb->offsets[tau + 1]; return; }
+    int64_t lo = 0, hi = n;                 /* first j with idx[j] >= offsets[tau] */
+    while (lo < hi) { int64_t m = (lo + hi) / 2; if (idx[m] < pb->offsets[tau]) lo = m + 1; else hi = m; }
+    *jb = lo;
+    hi = n;                                 /* first j with idx[j] >= offsets[tau+1] */
+    while (lo < hi) { int64_t m = (lo + hi) / 2; if (idx[m] < pb->offsets[tau + 1]) lo = m + 1; else hi = m; }
+    *je = lo;
+}
+
+/* The synchronization step (Algorithm 2, lines 10-12):
+ *   xbar_i  = (1/K) sum_k x_{k,i}
+ *   var_tau = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2      (pre-average x)
+ *   x_{k,i} = xbar_i for every k; momentum untouched.
+ * S = sum_tau var_tau is the paper's S_k (Var[.] of Section II-B with the squared
+ * norm).  Returns S; var_out[T] receives the per-tensor terms. */
+double orc_average(const orc_problem *pb, const int64_t *idx, int64_t n, double *x, double *var_out)
+{
+    const int32_t K = pb->K;
+    double *xbar = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j) {
+        double s = 0.0;
+        for (int32_t k = 0; k < K; ++k) s += x[(int64_t)k * n + j];
+        xbar[j] = s / (double)K;
+    }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int32_t tau = 0; tau < pb->T; ++tau) {
+        int64_t jb, je;
+        tensor_range(pb, idx, n, tau, &jb, &je);
+        double acc = 0.0;
+        for (int32_t k = 0; k < K; ++k)
+            for (int64_t j = jb; j < je; ++j) {
+                double dev = xbar[j] - x[(int64_t)k * n + j];
+                acc += dev * dev;
+            }
+        var_out[tau] = acc / (double)K;
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j)
+        for (int32_t k = 0; k < K; ++k) x[(int64_t)k * n + j] = xbar[j];
+    free(xbar);
+    double S = 0.0;
+    for (int32_t tau = 0; tau < pb->T; ++tau) S += var_out[tau];
+    return S;
+}
+
+/* Period controller after a sync at step t with variance S (Algorithm 2,
+ * lines 13-19).  Returns 0, or -4 if S is not finite (state unchanged). */
+int orc_controller(const orc_problem *pb, orc_state *st, int64_t t, double S)
+{
+    if (!isfinite(S)) return -4;
+    if (pb->period_mode != 1) return 0;
+    double gamma = orc_lr(pb, t);
+    if (t < pb->k_s) {
+        /* sampling phase: running (cumulative) mean of S / gamma */
+        st->nC2 += 1;
+        st->C2 += (S / gamma - st->C2) / (double)st->nC2;
+    } else if (S < pb->thr_lo * gamma * st->C2) {
+        st->p += 1;
+    } else if (S > pb->thr_hi * gamma * st->C2) {
+        if (st->p > 1) st->p -= 1;
+    }
+    return 0;
+}
+
+void orc_state_init(const orc_problem *pb, orc_state *st)
+{
+    memset(st, 0, sizeof(*st));
+    st->p = pb->p_init;
+}
+
+/* Run steps st->t .. st->t + n_steps - 1 of Algorithm 2 on the selection idx
+ * (idx NULL: all P elements; a strict subset is allowed only with a constant
+ * period, where the sync schedule does not depend on the data).
+ * x, v: [K][n], updated in place.  Each sync appends a record to log (up to
+ * log_cap) and its per-tensor variances to var_log[cap][T] (if non-NULL).
+ * Returns the number of syncs, or a negative error. */
+int64_t orc_run(const orc_problem *pb, const int64_t *idx, int64_t n, orc_state *st,
+                int64_t n_steps, const double *h, const double *xs, double *x, double *v,
+                orc_sync_rec *log, int64_t log_cap, double *var_log)
+{
+    if (idx && n != pb->P && pb->period_mode == 1) return -1;
+    double *var = (double *)malloc((size_t)pb->T * sizeof(double));
+    int64_t n_sync = 0;
+    for (int64_t s = 0; s < n_steps; ++s) {
+        int64_t t = st->t;
+        st->cnt += 1;
+        orc_local_step(pb, idx, n, t, h, xs, x, v);
+        if (st->cnt == st->p) {
+            st->cnt = 0;
+            double S = orc_average(pb, idx, n, x, var);
+            int32_t p_used = st->p;
+            int rc = orc_controller(pb, st, t, S);
+            if (n_sync < log_cap) {
+                if (log) {
+                    log[n_sync].t = t; log[n_sync].p = p_used;
+                    log[n_sync].S = S; log[n_sync].C2 = st->C2; log[n_sync].gamma = orc_lr(pb, t);
+                }
+                if (var_log) memcpy(var_log + n_sync * pb->T, var, (size_t)pb->T * sizeof(double));
+            }
+            n_sync += 1;
+            if (rc) { st->t = t + 1; free(var); return rc; }
+        }
+        st->t = t + 1;
+    }
+    free(var);
+    return n_sync;
+}
+
+/* The replica mean under any sync schedule.  Syncs replace each x_k by the mean
+ * and leave v alone, so they preserve both means; the dynamics are affine in
+ * (x, v), so the means follow one momentum-SGD run driven by the K-averaged
+ * noise: zbar = (1/K) sum_k z_k.  xbar, vbar: [n], updated in place. */
+void orc_mean_trajectory(const orc_problem *pb, const int64_t *idx, int64_t n, int64_t t0,
+                         int64_t n_steps, const double *h, const double *xs,
+                         double *xbar, double *vbar)
+{
+    for (int64_t t = t0; t < t0 + n_steps; ++t) {
+        double gamma = orc_lr(pb, t);
+#pragma omp parallel for schedule(static)
+        for (int64_t j = 0; j < n; ++j) {
+            int64_t i = idx ? idx[j] : j;
+            double zs = 0.0;
+            for (int32_t k = 0; k < pb->K; ++k) zs += noise(pb, k, t, i);
+            double zbar = zs / (double)pb->K;
+            double g = h[j] * (xbar[j] - xs[j]) + pb->sigma * zbar;
+            double d = g + pb->weight_decay * xbar[j];
+            vbar[j] = pb->momentum * vbar[j] + d;
+            xbar[j] = xbar[j] - gamma * vbar[j];
+        }
+    }
+}
+
+int orc_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

@@ -1,0 +1,392 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test checks the oracle against something other than itself: published
+known-answer values, the paper's printed numbers, closed forms of the linear
+dynamics, exact rational arithmetic, statistics of the noise law, or invariants
+of the averaging step.  A plausible mistake in the oracle (a dropped term, a
+wrong sign or index, a K-1 for a K, averaging the momentum) fails one of them.
+"""
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle
+from oracle import tiny_ref
+import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _tiny(K=4, sizes=(16,), **kw):
+    base = dict(name="tiny", K=K, sizes=tuple(sizes), seed=11, sigma=0.1, momentum=0.9,
+                weight_decay=0.0, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.05,
+                total_steps=40, period_mode=W.PERIOD_CONST, p_init=4, k_s=0)
+    base.update(kw)
+    return W.Workload(**base)
+
+
+# ---------------------------------------------------------------- generator
+
+def _kat():
+    rows = []
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                v = [int(s, 16) for s in line.split()]
+                rows.append((v[0:4], v[4:6], v[6:10]))
+    return rows
+
+
+def test_philox_known_answers():
+    for ctr, key, want in _kat():
+        assert oracle.philox4x32_10(ctr, key).tolist() == want
+        assert tiny_ref.philox4x32_10(ctr, key) == want
+
+
+def test_philox_c_matches_bigint_python():
+    rng = np.random.default_rng(5)
+    cases = [([0xFFFFFFFF, 0, 0, 0], [1, 0]), ([0xFFFFFFFF, 0xFFFFFFFF, 7, 1], [0, 0xFFFFFFFF])]
+    for _ in range(300):
+        cases.append((rng.integers(0, 2**32, 4, dtype=np.uint64).tolist(),
+                      rng.integers(0, 2**32, 2, dtype=np.uint64).tolist()))
+    for ctr, key in cases:
+        assert oracle.philox4x32_10(ctr, key).tolist() == tiny_ref.philox4x32_10(ctr, key)
+
+
+def test_philox_groups_use_group_as_first_counter_word():
+    seed = (3 << 32) | 17
+    out = oracle.philox_groups(seed, 5, 6, 2, g0=1000, n=8)
+    for j in range(8):
+        want = tiny_ref.philox4x32_10([1000 + j, 5, 6, 2], [17, 3])
+        assert out[j].tolist() == want
+
+
+def test_philox_output_words_are_uniform_bytes():
+    words = oracle.philox_groups(9, 1, 2, 0, 0, 1 << 16).ravel()
+    counts = np.bincount((words & 0xFF).astype(np.int64), minlength=256)
+    assert stats.chisquare(counts).pvalue > 1e-4
+    counts = np.bincount((words >> 24).astype(np.int64), minlength=256)
+    assert stats.chisquare(counts).pvalue > 1e-4
+
+
+def test_box_muller_special_values():
+    # u1 = 1 (all 24 top bits set): radius sqrt(-2 ln 1) = 0.
+    assert np.all(oracle.box_muller(0xFFFFFFFF, 0x12345678) == 0.0)
+    # u1 = 2^-24, u2 = 0: z0 = sqrt(48 ln 2), z1 = 0.
+    z = oracle.box_muller(0, 0)
+    assert z[0] == pytest.approx(np.sqrt(48 * np.log(2.0)), rel=1e-15) and z[1] == 0.0
+    # u2 = 1/4: angle pi/2, so z0 ~ 0 and z1 = radius; u2 = 1/2: z0 = -radius.
+    r = np.sqrt(-2.0 * np.log((0x800000 + 1) / 2**24))
+    z = oracle.box_muller(0x80000000, 0x40000000)
+    assert abs(z[0]) < 1e-15 and z[1] == pytest.approx(r, rel=1e-15)
+    z = oracle.box_muller(0x80000000, 0x80000000)
+    assert z[0] == pytest.approx(-r, rel=1e-15) and abs(z[1]) < 1e-15
+
+
+def test_normals_are_standard_normal():
+    z = oracle.normals_groups(1234, 3, 77, 0, 0, 250_000)
+    assert abs(z.mean()) < 5 / np.sqrt(z.size)
+    assert abs(z.var() - 1.0) < 5 * np.sqrt(2.0 / z.size)
+    assert abs(stats.kurtosis(z, fisher=False) - 3.0) < 0.03
+    assert stats.kstest(z, "norm").pvalue > 1e-3
+    # the two members of a Box-Muller pair are uncorrelated
+    assert abs(np.corrcoef(z[0::2], z[1::2])[0, 1]) < 5 / np.sqrt(z.size / 2)
+
+
+def test_problem_data_laws():
+    w = _tiny(sizes=(200_000,), h_lo=1e-3, h_hi=1.0)
+    h, xs = oracle.problem_data(w)
+    assert h.min() >= 1e-3 * (1 - 1e-12) and h.max() <= 1.0
+    u = (np.log(h) - np.log(1e-3)) / (np.log(1.0) - np.log(1e-3))
+    assert stats.kstest(u, "uniform").pvalue > 1e-3
+    assert stats.kstest(xs, "norm").pvalue > 1e-3
+    # a subset selection returns the same values as the full draw
+    idx = np.array([0, 3, 4, 77, 199_999])
+    hs, xss = oracle.Oracle(w).problem_data(idx)
+    assert np.array_equal(hs, h[idx]) and np.array_equal(xss, xs[idx])
+
+
+# ---------------------------------------------------------------- schedule and controller
+
+def _facts(kind):
+    out = []
+    with open(os.path.join(GOLDEN, "paper_schedule_facts.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                p = line.split()
+                if p[0] == kind:
+                    out.append(p[1:])
+    return out
+
+
+def test_learning_rate_step_decay_matches_paper():
+    for N, t, ratio in _facts("lr_step"):
+        w = _tiny(lr_kind=W.LR_STEP, lr0=0.1, total_steps=int(N))
+        assert oracle.lr(w, int(t)) == pytest.approx(0.1 * float(ratio), rel=1e-12)
+
+
+def test_learning_rate_cosine_special_points():
+    w = _tiny(lr_kind=W.LR_COSINE, lr0=0.1, total_steps=1000)
+    assert oracle.lr(w, 0) == pytest.approx(0.1, rel=1e-15)
+    assert oracle.lr(w, 500) == pytest.approx(0.05, rel=1e-12)
+    assert oracle.lr(w, 250) == pytest.approx(0.05 * (1 + np.sqrt(0.5)), rel=1e-12)
+    assert oracle.lr(w, 999) > 0
+
+
+def test_sync_counts_match_paper():
+    for phases, want in _facts("syncs"):
+        total = 0
+        for ph in phases.split(","):
+            steps, p = (int(v) for v in ph.split(":"))
+            w = _tiny(total_steps=steps, p_init=p, period_mode=W.PERIOD_CONST)
+            syncs, _ = oracle.controller_trace(w, lambda t, g: 1.0)
+            # Algorithm 2's counter: syncs after 0-based steps p-1, 2p-1, ...
+            assert [t for t, _ in syncs] == list(range(p - 1, steps, p))
+            total += len(syncs)
+        assert total == int(want)
+
+
+def test_algorithm2_constants():
+    f = {k: float(v) for k, v in _facts("alg2")}
+    w = W.full_workloads()["resnet50_like"]
+    assert (w.thr_lo, w.thr_hi) == (f["thr_lo"], f["thr_hi"])
+    assert w.p_init == f["p_init"] and w.k_s == int(f["k_s_fraction"] * w.total_steps)
+
+
+def _adaptive(**kw):
+    base = dict(total_steps=400, period_mode=W.PERIOD_ADAPTIVE, p_init=4, k_s=100)
+    base.update(kw)
+    return _tiny(**base)
+
+
+def test_controller_sampling_phase_keeps_p_and_averages():
+    w = _adaptive()
+    vals = iter([3.0, 5.0, 10.0, 2.0] + [0.0] * 1000)
+    syncs, st = oracle.controller_trace(w, lambda t, g: next(vals) * g)
+    # first 25 syncs (t = 3, 7, ..., 99) are in the sampling phase: p stays 4
+    assert [p for t, p in syncs if t < 100] == [4] * 25
+    # C2 is the plain mean of S/gamma over the sampling syncs
+    assert st.C2 == pytest.approx((3 + 5 + 10 + 2 + 0 * 21) / 25, rel=1e-14)
+
+
+def test_controller_zero_variance_grows_period_each_sync():
+    w = _adaptive()
+    syncs, st = oracle.controller_trace(w, lambda t, g: (1.0 * g if t < 100 else 0.0))
+    after = [(t, p) for t, p in syncs if t >= 100]
+    # p grows by one per sync: gaps 4, 5, 6, ... after the sampling phase
+    t_prev = 99
+    for j, (t, p) in enumerate(after):
+        assert p == 4 + j and t - t_prev == p
+        t_prev = t
+
+
+def test_controller_huge_variance_clamps_period_at_one():
+    w = _adaptive()
+    syncs, st = oracle.controller_trace(w, lambda t, g: (1.0 * g if t < 100 else 1e9))
+    after = [p for t, p in syncs if t >= 100]
+    assert after[:4] == [4, 3, 2, 1] and set(after[4:]) == {1}
+    assert st.p == 1
+
+
+def test_controller_band_keeps_period():
+    w = _adaptive()
+    # S/gamma == C2 exactly, also across thresholds 0.7..1.3 (strict comparisons)
+    for ratio in (1.0, 0.7, 1.3):
+        syncs, st = oracle.controller_trace(w, lambda t, g: (2.0 * g if t < 100 else ratio * 2.0 * g))
+        assert {p for _, p in syncs} == {4}
+    syncs, _ = oracle.controller_trace(w, lambda t, g: (2.0 * g if t < 100 else 0.69 * 2.0 * g))
+    assert max(p for _, p in syncs) > 4
+    syncs, _ = oracle.controller_trace(w, lambda t, g: (2.0 * g if t < 100 else 1.31 * 2.0 * g))
+    assert min(p for _, p in syncs) < 4
+
+
+def test_controller_rejects_non_finite_and_keeps_state():
+    w = _adaptive()
+    o = oracle.Oracle(w)
+    st = o.new_state()
+    st.p = 6
+    st.C2 = 2.5
+    st.nC2 = 3
+    for bad in (float("nan"), float("inf")):
+        assert o.controller(st, 200, bad) == -4
+        assert (st.p, st.C2, st.nC2) == (6, 2.5, 3)
+
+
+# ---------------------------------------------------------------- step dynamics
+
+def _heavy_ball_closed_form(h, xs, a, gamma, mu, N):
+    """x, v after N steps from 0 of v' = mu v + a x - h x*, x' = x - gamma v'."""
+    xs_out, vs_out = np.zeros_like(h), np.zeros_like(h)
+    for j in range(len(h)):
+        A = np.array([[1 - gamma * a[j], -gamma * mu], [a[j], mu]])
+        b = np.array([gamma * h[j] * xs[j], -h[j] * xs[j]])
+        s_fix = np.array([h[j] * xs[j] / a[j], 0.0])       # fixed point: v = 0, a x = h x*
+        assert np.allclose(A @ s_fix + b, s_fix)
+        s = np.linalg.matrix_power(A, N) @ (np.zeros(2) - s_fix) + s_fix
+        xs_out[j], vs_out[j] = s
+    return xs_out, vs_out
+
+
+@pytest.mark.parametrize("wd", [0.0, 5e-4])
+def test_noise_free_run_is_heavy_ball_closed_form(wd):
+    w = _tiny(K=3, sizes=(7, 9), sigma=0.0, weight_decay=wd, total_steps=60, p_init=1000)
+    r = oracle.Oracle(w).run()
+    x_cf, v_cf = _heavy_ball_closed_form(r.h, r.xs, r.h + wd, w.lr0, w.momentum, 60)
+    for k in range(3):
+        np.testing.assert_allclose(r.x[k], x_cf, rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(r.v[k], v_cf, rtol=1e-11, atol=1e-13)
+    assert r.n_syncs == 0
+
+
+def test_exact_rational_run_bounds_rounding():
+    w = _tiny(K=3, sizes=(2, 3, 1), sigma=0.3, weight_decay=5e-4, total_steps=7, p_init=3,
+              lr_kind=W.LR_STEP, lr0=0.2)
+    o = oracle.Oracle(w)
+    r = o.run()
+    P = w.P
+    noise = []
+    for t in range(w.total_steps):
+        per_k = []
+        for k in range(w.K):
+            z = oracle.normals_groups(w.seed, k, t, 0, 0, (P + 3) // 4)[:P]
+            per_k.append(z.tolist())
+        noise.append(per_k)
+    lrs = [o.lr(t) for t in range(w.total_steps)]
+    x, v, syncs = tiny_ref.exact_run(w.K, P, list(w.offsets()), r.h.tolist(), r.xs.tolist(), noise,
+                                     w.sigma, w.momentum, w.weight_decay, lrs, {2, 5})
+    np.testing.assert_allclose(r.x, np.array(x, dtype=float), rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(r.v, np.array(v, dtype=float), rtol=1e-13, atol=1e-15)
+    assert list(r.sync_t) == [t for t, _ in syncs]
+    np.testing.assert_allclose(r.var, np.array([[float(q) for q in var] for _, var in syncs]),
+                               rtol=1e-11)
+
+
+# ---------------------------------------------------------------- averaging step
+
+def test_variance_identity_in_long_double():
+    w = _tiny(K=5, sizes=(3, 10, 1, 50))
+    o = oracle.Oracle(w)
+    rng = np.random.default_rng(2)
+    x = rng.normal(size=(5, w.P)) * rng.uniform(0.1, 3.0, size=w.P)
+    xl = x.astype(np.longdouble)
+    S, var = o.average(x.copy())
+    off = w.offsets()
+    for tau in range(w.T):
+        seg = xl[:, off[tau]:off[tau + 1]]
+        xbar = seg.mean(axis=0)
+        want = (seg ** 2).sum() / 5 - (xbar ** 2).sum()
+        assert var[tau] == pytest.approx(float(want), rel=1e-9, abs=1e-12)
+    assert S == pytest.approx(var.sum(), rel=1e-15)
+
+
+def test_average_broadcasts_mean_and_is_idempotent():
+    w = _tiny(K=4, sizes=(5, 6))
+    o = oracle.Oracle(w)
+    x = np.random.default_rng(3).normal(size=(4, w.P))
+    mean = x.mean(axis=0)
+    S1, _ = o.average(x)
+    assert S1 > 0
+    for k in range(4):
+        np.testing.assert_allclose(x[k], mean, rtol=1e-15, atol=1e-16)
+        assert np.array_equal(x[k], x[0])
+    S2, var2 = o.average(x)
+    assert S2 == 0.0 and np.all(var2 == 0.0)
+
+
+def test_single_worker_has_zero_variance():
+    w = _tiny(K=1, sizes=(33, 31), total_steps=50, period_mode=W.PERIOD_ADAPTIVE, k_s=10)
+    r = oracle.Oracle(w).run()
+    assert r.n_syncs > 0 and np.all(r.var == 0.0) and np.all(r.S == 0.0)
+
+
+def test_variance_is_independent_of_optimum():
+    w = _tiny(K=4, sizes=(40, 24), weight_decay=5e-4, total_steps=30, p_init=5)
+    o = oracle.Oracle(w)
+    r1 = o.run()
+    r2 = o.run(xs=r1.xs + 3.0)
+    np.testing.assert_allclose(r2.var, r1.var, rtol=1e-7)
+
+
+def test_period_one_replicas_follow_averaged_gradient_sgd():
+    # p = 1: every step ends with a sync, so all replicas equal the mean, and the
+    # mean is plain momentum SGD on the K-averaged gradient (FULLSGD).
+    w = _tiny(K=4, sizes=(30,), p_init=1, total_steps=25, weight_decay=5e-4)
+    o = oracle.Oracle(w)
+    r = o.run()
+    for k in range(1, 4):
+        assert np.array_equal(r.x[k], r.x[0])
+    xbar, vbar = o.mean_trajectory(25, h=r.h, xs=r.xs)
+    np.testing.assert_allclose(r.x[0], xbar, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(r.v.mean(axis=0), vbar, rtol=1e-10, atol=1e-13)
+
+
+@pytest.mark.parametrize("mode", [W.PERIOD_CONST, W.PERIOD_ADAPTIVE])
+def test_mean_trajectory_is_schedule_independent(mode):
+    w = _tiny(K=4, sizes=(13, 51), total_steps=80, period_mode=mode, p_init=3, k_s=20,
+              weight_decay=5e-4, lr_kind=W.LR_COSINE, lr0=0.1)
+    o = oracle.Oracle(w)
+    r = o.run()
+    xbar, vbar = o.mean_trajectory(80, h=r.h, xs=r.xs)
+    np.testing.assert_allclose(r.x.mean(axis=0), xbar, rtol=1e-11, atol=1e-13)
+    np.testing.assert_allclose(r.v.mean(axis=0), vbar, rtol=1e-10, atol=1e-12)
+
+
+def test_subset_run_matches_full_run():
+    w = _tiny(K=3, sizes=(100, 57), total_steps=20, p_init=6, weight_decay=5e-4)
+    o = oracle.Oracle(w)
+    full = o.run()
+    idx = np.array([0, 1, 5, 99, 100, 101, 156])
+    sub = o.run(idx=idx)
+    np.testing.assert_array_equal(sub.x, full.x[:, idx])
+    np.testing.assert_array_equal(sub.v, full.v[:, idx])
+    assert list(sub.sync_t) == list(full.sync_t)
+
+
+# ---------------------------------------------------------------- statistics of S
+
+def _expected_sync_variance(h, wd, gamma, mu, sigma, K, sync_steps, N):
+    """E[S] before each sync: propagate the covariance of each element's
+    deviation pair (e, u) = (x_k - xbar, v_k - vbar).  The deviation noise
+    sigma (z_k - zbar) has variance sigma^2 (K-1)/K; a sync zeroes e (and its
+    covariance with u) but keeps u, since momentum is not averaged."""
+    a = h + wd
+    Cee = np.zeros_like(h); Ceu = np.zeros_like(h); Cuu = np.zeros_like(h)
+    q = sigma * sigma * (K - 1) / K
+    out = []
+    for t in range(N):
+        # u' = mu u + a e + xi ;  e' = e - gamma u'
+        uu = mu * mu * Cuu + 2 * mu * a * Ceu + a * a * Cee + q
+        ue = mu * Ceu + a * Cee            # Cov(u', e)
+        Cuu_n = uu
+        Ceu_n = ue - gamma * uu            # Cov(e', u') = Cov(e,u') - gamma Var(u')
+        Cee_n = Cee - 2 * gamma * ue + gamma * gamma * uu
+        Cee, Ceu, Cuu = Cee_n, Ceu_n, Cuu_n
+        if t in sync_steps:
+            out.append(Cee.sum())
+            Cee = np.zeros_like(h); Ceu = np.zeros_like(h)
+    return np.array(out)
+
+
+@pytest.mark.parametrize("mu,wd,p", [(0.0, 0.0, 1), (0.0, 0.0, 3), (0.0, 0.0, 8),
+                                     (0.9, 5e-4, 3), (0.9, 0.0, 8)])
+def test_sync_variance_matches_closed_form(mu, wd, p):
+    K, P, R, N = 4, 2048, 40, 4 * p
+    w0 = _tiny(K=K, sizes=(P,), momentum=mu, weight_decay=wd, sigma=0.1, lr0=0.1,
+               total_steps=N, p_init=p)
+    h, _ = oracle.problem_data(w0)
+    sync_steps = set(range(p - 1, N, p))
+    want = _expected_sync_variance(h, wd, 0.1, mu, 0.1, K, sync_steps, N)
+    if mu == 0.0 and wd == 0.0:
+        # plain SGD: E[S] = (K-1)/K gamma^2 sigma^2 sum_i sum_{t<p} (1 - gamma h_i)^(2t)
+        plain = (K - 1) / K * 0.01 * 0.01 * sum(((1 - 0.1 * h) ** (2 * t)).sum() for t in range(p))
+        np.testing.assert_allclose(want, plain, rtol=1e-12)
+    samples = []
+    for r in range(R):
+        w = w0.replace(seed=1000 + r)
+        samples.append(oracle.Oracle(w).run(h=h).S)   # same curvatures, fresh noise
+    samples = np.array(samples)
+    mean = samples.mean(axis=0)
+    se = samples.std(axis=0, ddof=1) / np.sqrt(R)
+    assert np.all(np.abs(mean - want) < 4 * se + 1e-12), (mean, want, se)
