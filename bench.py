@@ -1,0 +1,163 @@
+"""Throughput of the ADPSGD hot path on one MI355X.
+
+One bench step is one whole ADPSGD run of the 138M-parameter workload
+(K = 8 workers, P = 138,000,000 fp32 parameters in 32 tensors, 500 local
+steps, adaptive period from p = 4 with C2 sampled over the first 125 steps):
+every local step, every fused sync (mean, broadcast, per-tensor variance) and
+every controller decision.  The replicas and momentum buffers are reset to
+zero at the start of each run; h and x* stay resident in HBM.
+
+Metric: parameter-updates/s = K * P * 500 * steps / time.  The roofline entry
+is for the dominant kernel (the plain local step): algorithmic bytes per
+launch (16 K P + 8 P) over its mean duration from HIP events recorded on the
+library's stream during the timed region.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "local_step_k8_p138m_traffic.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2007_06134_amd", "csrc", "kernels.hip")
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for name in ("kernels.hip", "rng.hpp", "kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2007_06134_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per local-step launch from the committed counter summary, if it
+    was taken on the current kernel sources; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    txt = open(TRAFFIC_FILE).read()
+    m_d = re.search(r"kernel sources digest:\s*`?([0-9a-f]{16})", txt)
+    m_b = re.search(r"HBM bytes per launch \(scaled\):\s*([0-9.eE+]+)", txt)
+    if not (m_d and m_b) or m_d.group(1) != kernel_source_digest():
+        return None
+    return float(m_b.group(1))
+
+
+def cpu_baseline(w, P_sample=4_000_000, steps=40):
+    """The oracle, as it stands, on the first P_sample parameters of the same workload."""
+    import oracle
+    import workloads as W
+    # keep whole tensors that fit, then cut the one that crosses P_sample
+    sizes, acc = [], 0
+    for s in w.sizes:
+        take = min(s, P_sample - acc)
+        if take <= 0:
+            break
+        sizes.append(take)
+        acc += take
+    ws = w.replace(name=w.name + "_cpu_sample", sizes=tuple(sizes))
+    o = oracle.Oracle(ws)
+    h, xs = o.problem_data()
+    t0 = time.perf_counter()
+    o.run(n_steps=steps, h=h, xs=xs)
+    dt = time.perf_counter() - t0
+    return {
+        "value": ws.K * ws.P * steps / dt, "unit": "param-updates/s", "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"first {ws.P:,} of {w.P:,} parameters (K={w.K}), steps 0-{steps - 1} of the same "
+                  f"adaptive run, fp64, {dt:.1f} s",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="vgg16_adaptive")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-timing", action="store_true", help="skip per-kernel HIP events")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (the K workers share one GPU's HBM); "
+              "--gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    import paper_2007_06134_amd as A
+
+    w = W.full_workloads()[args.workload]
+    N = w.total_steps
+    eng = A.Adpsgd.from_workload(w, device="cuda:0")
+    stream = eng.stream
+
+    def one_run():
+        eng.reset()
+        return eng.run(N, log_cap=N, with_var=False)
+
+    for _ in range(args.warmup):
+        one_run()
+    torch.cuda.synchronize()
+    eng.set_timing(not args.no_timing)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n_syncs = []
+    for _ in range(args.steps):
+        recs, _, n = one_run()
+        n_syncs.append(n)
+    stream.synchronize()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tm = eng.get_timing()
+    eng.close()
+
+    updates = w.K * w.P * N * args.steps
+    step_bytes = 16 * w.K * w.P + 8 * w.P          # x, m read+write per worker; h, x* once
+    out = {
+        "metric": "param-updates/s",
+        "value": updates / elapsed,
+        "unit": "param-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "K": w.K, "P": w.P, "T": w.T, "local_steps_per_run": N,
+                   "period": "adaptive, p_init 4, K_s 125, thresholds 0.7/1.3",
+                   "syncs_per_run": int(n_syncs[-1])},
+    }
+    if tm.step_launches > 0:
+        step_ms = tm.step_ms / tm.step_launches
+        achieved = step_bytes / (step_ms * 1e-3) / 1e9
+        out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                           "kernel": "k_local_step", "bytes_per_launch": step_bytes,
+                           "avg_launch_ms": step_ms}
+        if tm.fused_launches > 0:
+            fused_ms = tm.fused_ms / tm.fused_launches
+            out["fused_step_sync"] = {"avg_launch_ms": fused_ms,
+                                      "achieved_GBs": step_bytes / (fused_ms * 1e-3) / 1e9,
+                                      "segsum_avg_ms": tm.segsum_ms / max(tm.segsum_launches, 1)}
+        out["hbm_GBs_whole_run"] = (step_bytes * N * args.steps) / elapsed / 1e9
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

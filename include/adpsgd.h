@@ -1,0 +1,228 @@
+/*
+ * adpsgd.h -- C ABI of the MI355X (gfx950) ADPSGD hot path.
+ *
+ * ADPSGD is adaptive periodic parameter averaging SGD (Jiang and Agrawal,
+ * arXiv 2007.06134, Algorithm 2).  K simulated workers keep stacked fp32
+ * parameter replicas x[K][P] and momentum buffers m[K][P] in one GPU's HBM.
+ * Each local step applies momentum SGD to every replica with a noisy diagonal
+ * quadratic gradient; every p steps the replicas are averaged, the
+ * inter-worker parameter variance is reduced per tensor, and a host controller
+ * moves p to keep that variance near gamma * C2.
+ *
+ * Conventions shared by every call:
+ *   - Every call returns an int status: ADPSGD_OK (0) or a negative code below.
+ *     adpsgd_last_error() gives a message for the calling thread's last error.
+ *   - Arguments are validated before anything is enqueued; on a validation
+ *     error nothing runs and the context is unchanged.
+ *   - Device buffers are caller-owned (the library never allocates or frees
+ *     them).  Host arrays are read during the call and never retained, except
+ *     where stated.
+ *   - One context is used by one host thread at a time.
+ *   - Step indices t are 0-based: step t is the paper's iteration k = t.
+ *
+ * Readings of points the paper leaves open, used throughout:
+ *   - The sync follows Algorithm 2's counter in both period modes: syncs
+ *     happen after 0-based steps p-1, 2p-1, ... (a constant period is
+ *     Algorithm 2 with no controller updates).
+ *   - Momentum buffers stay local; only parameters are averaged.
+ *   - RunningAverage(C2, S/gamma) is the cumulative mean over sampling syncs.
+ *   - p stays within [1, p_max].
+ *   - Variance: (1/K) sum_k sum_{i in tensor} (xbar_i - x_{k,i})^2, taken on
+ *     the replicas just before they are replaced by their mean.
+ */
+#ifndef ADPSGD_H
+#define ADPSGD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Only the functions below are exported from the shared library. */
+#define ADPSGD_API __attribute__((visibility("default")))
+
+/* ---- status codes ---------------------------------------------------------- */
+#define ADPSGD_OK 0
+#define ADPSGD_EINVAL (-1)     /* invalid argument; nothing was enqueued           */
+#define ADPSGD_ESTATE (-2)     /* call not valid in the context's current state    */
+#define ADPSGD_EDEVICE (-3)    /* a HIP runtime call failed (see adpsgd_last_error) */
+#define ADPSGD_ENONFINITE (-4) /* the variance S was NaN or infinite; p unchanged  */
+
+/* ---- learning-rate schedules: gamma_t for 0-based step t ------------------- */
+#define ADPSGD_LR_CONST 0  /* gamma_t = lr0                                             */
+#define ADPSGD_LR_STEP 1   /* lr0 * 0.1 from t = floor(N/2), * 0.01 from floor(3N/4);
+                              the paper's 10x decays at 1/2 and 3/4 of training (Sec. IV-B) */
+#define ADPSGD_LR_COSINE 2 /* lr0 * (1 + cos(pi t / N)) / 2                              */
+
+/* ---- period modes ----------------------------------------------------------- */
+#define ADPSGD_PERIOD_CONST 0    /* CPSGD, Algorithm 1: p = p_init throughout            */
+#define ADPSGD_PERIOD_ADAPTIVE 1 /* ADPSGD, Algorithm 2: C2 sampling, then p +- 1        */
+
+typedef struct adpsgd_ctx adpsgd_ctx; /* opaque, owned by the library */
+
+/* Hyper-parameters (Algorithm 2's Require line: p_init, K_s; Section IV-A:
+ * momentum; the noisy quadratic stand-in for the mini-batch gradient of
+ * eq. (3): g_k = h * (x_k - x*) + sigma * z_k, z_k ~ N(0,1) from Philox4x32-10
+ * keyed by seed with counter (i/4, k, t, 0); h ~ LogUniform[h_lo, h_hi]
+ * (counter tag 1) and x* ~ N(0,1) (tag 2) per element). */
+typedef struct {
+    uint64_t seed;
+    double sigma;        /* noise standard deviation, >= 0                       */
+    double momentum;     /* heavy-ball coefficient, in [0, 1)                     */
+    double weight_decay; /* coupled L2: d = g + weight_decay * x, >= 0            */
+    double h_lo, h_hi;   /* curvature range, 0 < h_lo <= h_hi                     */
+    int32_t lr_kind;     /* ADPSGD_LR_*                                           */
+    int32_t period_mode; /* ADPSGD_PERIOD_*                                       */
+    double lr0;          /* base learning rate, > 0                               */
+    int64_t total_steps; /* N: the schedule's length (step decay / cosine), >= 1  */
+    int32_t p_init;      /* initial (or constant) averaging period, >= 1          */
+    int32_t p_max;       /* upper bound on p; 0 means INT32_MAX                   */
+    int64_t k_s;         /* syncs after steps t < k_s sample C2 (Alg. 2, l. 13)   */
+    double thr_lo;       /* p += 1 if S < thr_lo * gamma_t * C2 (paper: 0.7)      */
+    double thr_hi;       /* p -= 1 if S > thr_hi * gamma_t * C2 (paper: 1.3)      */
+} adpsgd_hparams;
+
+/* Caller-owned device memory, on the device current at adpsgd_init. */
+typedef struct {
+    float *x;               /* [K][P] replicas, row-major, 16-byte aligned; zeroed by init */
+    float *m;               /* [K][P] momentum buffers, same layout; zeroed by init          */
+    float *h;               /* [P] curvatures, written by init                               */
+    float *xstar;           /* [P] optimum, written by init                                  */
+    void *workspace;        /* >= adpsgd_workspace_bytes(...) bytes, 256-byte aligned;
+                               tile table, tile partials and the variance ring                */
+    size_t workspace_bytes;
+    void *stream;           /* hipStream_t for every launch and copy; NULL = null stream     */
+} adpsgd_buffers;
+
+/* Controller state on the host (Algorithm 2, lines 1-3).  x and m are the
+ * device part of the state and stay in the caller's buffers. */
+typedef struct {
+    int64_t t;       /* next step index                          */
+    int64_t cnt;     /* steps since the last sync (Alg. 2 cnt)   */
+    int64_t nC2;     /* sampling syncs folded into C2            */
+    double C2;       /* sampled constant C2                      */
+    int32_t p;       /* current averaging period                 */
+    int32_t reserved;
+} adpsgd_state;
+
+/* One record per synchronization. */
+typedef struct {
+    int64_t t;       /* the sync followed step t                               */
+    int32_t p;       /* period in force for this sync                          */
+    int32_t reserved;
+    double S;        /* sum over tensors of the per-tensor variance (S_k)      */
+    double C2;       /* C2 after this sync                                     */
+    double gamma;    /* learning rate of step t                                */
+    double margin;   /* signed relative distance of S to the nearer threshold,
+                        S / (thr * gamma * C2) - 1; NaN when no decision made  */
+} adpsgd_sync_rec;
+
+/* Per-kernel device time, from HIP events around each launch when enabled. */
+typedef struct {
+    double step_ms;     int64_t step_launches;     /* plain local step            */
+    double fused_ms;    int64_t fused_launches;    /* last step of a period + sync */
+    double average_ms;  int64_t average_launches;  /* separate mean/broadcast/var */
+    double segsum_ms;   int64_t segsum_launches;   /* per-tensor variance sums    */
+} adpsgd_timing;
+
+/* Bytes of device workspace for K workers, P parameters and T tensors with
+ * boundaries offsets[0..T] (host).  Returns 0 if the arguments are invalid. */
+ADPSGD_API size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const int64_t *offsets);
+
+/* Create a context (Algorithm 2, lines 1-3, and w_{0,i} = w_0 = 0).
+ * K >= 1 workers; P >= 0 parameters; T >= 1 tensors with host offsets[T+1],
+ * non-decreasing, offsets[0] = 0, offsets[T] = P (empty tensors allowed).
+ * Fills h and xstar from the seed, zeroes x and m, and waits for the stream.
+ * P/4 and the step count must stay below 2^32 (Philox counter words). */
+ADPSGD_API int adpsgd_init(int32_t K, int64_t P, const int64_t *tensor_offsets, int32_t T,
+                const adpsgd_hparams *hp, const adpsgd_buffers *buf, adpsgd_ctx **out);
+
+/* Zero x and m and reset the controller state to t = 0, cnt = 0, p = p_init,
+ * C2 = 0.  h and xstar are kept.  Asynchronous. */
+ADPSGD_API int adpsgd_reset(adpsgd_ctx *c);
+
+/* Enqueue n >= 0 plain local steps t .. t+n-1 on every worker (Algorithm 2,
+ * lines 5-7): d = h (x - x*) + sigma z + wd x; m = mu m + d; x = x - gamma_t m.
+ * Advances t and cnt by n.  Asynchronous. */
+ADPSGD_API int adpsgd_local_steps(adpsgd_ctx *c, int32_t n);
+
+/* Synchronize now (Algorithm 2, lines 9-12): xbar = mean of the K replicas,
+ * var_out[tau] = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2 (host, [T],
+ * fp64), every replica set to xbar, momentum untouched, cnt = 0.  Blocks until
+ * var_out is valid. */
+ADPSGD_API int adpsgd_average(adpsgd_ctx *c, double *var_out);
+
+/* One local step followed by the synchronization, in a single pass over x and
+ * m (same results as adpsgd_local_steps(c, 1) then adpsgd_average).  Blocks. */
+ADPSGD_API int adpsgd_step_average(adpsgd_ctx *c, double *var_out);
+
+/* Period controller (Algorithm 2, lines 13-19) for a sync after step t - 1 with
+ * S = sum(var[0..T)).  Sampling phase (t-1 < k_s): C2 <- running mean of
+ * S / gamma; otherwise p + 1 if S < thr_lo gamma C2, p - 1 if S > thr_hi
+ * gamma C2.  Constant mode: no change.  *next_period (may be NULL) receives p.
+ * ENONFINITE, with the state unchanged, if S is NaN or infinite. */
+ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_period);
+
+/* Run n_steps steps of Algorithm 2 from the current state: local steps, a sync
+ * whenever cnt reaches p (fused into that period's last step), and the
+ * controller after every sync.  log (host, log_cap records) and var_log (host,
+ * [log_cap][T], may be NULL) receive the first log_cap syncs; *n_syncs (may be
+ * NULL) the count of all syncs.  No sync is forced at the end.  Returns when
+ * all enqueued work has finished.  On ENONFINITE the run stops at that sync;
+ * steps already enqueued after it complete and are counted in the state. */
+ADPSGD_API int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
+               double *var_log, int64_t *n_syncs);
+
+ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
+/* Restore a state saved by adpsgd_get_state (x, m restored by the caller):
+ * t >= 0, cnt >= 0, nC2 >= 0, 1 <= p <= p_max, C2 finite. */
+ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
+
+/* Per-kernel HIP-event timing (off by default).  Turning it on or reading it
+ * waits for the stream. */
+ADPSGD_API int adpsgd_set_timing(adpsgd_ctx *c, int32_t on);
+ADPSGD_API int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out);
+
+/* Release the context (host memory and events).  Waits for the stream.  The
+ * caller's device buffers are untouched.  NULL is accepted. */
+ADPSGD_API int adpsgd_destroy(adpsgd_ctx *c);
+
+/* Message for the calling thread's last failed call (empty if none). */
+ADPSGD_API const char *adpsgd_last_error(void);
+
+/* ---- generator dumps (the device code the steps use) ------------------------ */
+
+/* dev_out[4j .. 4j+3] = Philox4x32-10(key = (seed mod 2^32, seed >> 32),
+ * counter = (g0 + j, c1, c2, c3)) for j < n_groups; device uint32 [4 n_groups].
+ * Asynchronous on stream. */
+ADPSGD_API int adpsgd_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0,
+                       int64_t n_groups, uint32_t *dev_out, void *stream);
+
+/* dev_out[4j .. 4j+3] = the four Box-Muller normals of the same words:
+ * (z0, z1) = sqrt(-2 ln u1) (cos 2 pi u2, sin 2 pi u2) with
+ * u1 = ((r0 >> 8) + 1) 2^-24, u2 = (r1 >> 8) 2^-24, and likewise (z2, z3)
+ * from (r2, r3).  Device float [4 n_groups].  Asynchronous on stream. */
+ADPSGD_API int adpsgd_normal_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0,
+                       int64_t n_groups, float *dev_out, void *stream);
+
+/* ---- host-only controller (no GPU needed) ------------------------------------ */
+
+/* Learning rate gamma_t of 0-based step t under hp's schedule. */
+ADPSGD_API double adpsgd_lr(const adpsgd_hparams *hp, int64_t t);
+
+/* Initial controller state: t = cnt = nC2 = 0, C2 = 0, p = p_init. */
+ADPSGD_API int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st);
+
+/* Apply Algorithm 2, lines 13-19, for a sync after step t with variance S;
+ * *margin (may be NULL) receives the decision margin (NaN if no decision).
+ * Updates st->p, st->C2, st->nC2 only.  ENONFINITE (state unchanged) if S is
+ * not finite; EINVAL on a NULL pointer. */
+ADPSGD_API int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
+                         double *margin);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ADPSGD_H */

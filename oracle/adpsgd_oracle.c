@@ -202,14 +202,6 @@ void orc_problem_data(const orc_problem *pb, const int64_t *idx, int64_t n, doub
     }
 }
 
-/* Gradient noise z for worker k, step t, element i. */
-static double noise(const orc_problem *pb, int32_t k, int64_t t, int64_t i)
-{
-    double z[4];
-    orc_normals4(pb->seed, (uint32_t)(i / 4), (uint32_t)k, (uint32_t)t, 0, z);
-    return z[i % 4];
-}
-
 /* One local step t on every worker (Algorithm 2, lines 6-7, with heavy-ball
  * momentum as in PyTorch SGD: d = g + wd*x; v = mu*v + d; x = x - gamma*v).
  * x and v are [K][n] over the selected elements idx[0..n) (all if idx NULL). */
@@ -364,20 +356,36 @@ void orc_mean_trajectory(const orc_problem *pb, const int64_t *idx, int64_t n, i
                          int64_t n_steps, const double *h, const double *xs,
                          double *xbar, double *vbar)
 {
+    double *zsum = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
     for (int64_t t = t0; t < t0 + n_steps; ++t) {
         double gamma = orc_lr(pb, t);
+        for (int64_t j = 0; j < n; ++j) zsum[j] = 0.0;
+        for (int32_t k = 0; k < pb->K; ++k) {
+#pragma omp parallel
+            {
+                int64_t g_memo = -1;              /* one generator call per group */
+                double z4[4] = {0, 0, 0, 0};
+#pragma omp for schedule(static)
+                for (int64_t j = 0; j < n; ++j) {
+                    int64_t i = idx ? idx[j] : j;
+                    if (i / 4 != g_memo) {
+                        g_memo = i / 4;
+                        orc_normals4(pb->seed, (uint32_t)g_memo, (uint32_t)k, (uint32_t)t, 0, z4);
+                    }
+                    zsum[j] += z4[i % 4];
+                }
+            }
+        }
 #pragma omp parallel for schedule(static)
         for (int64_t j = 0; j < n; ++j) {
-            int64_t i = idx ? idx[j] : j;
-            double zs = 0.0;
-            for (int32_t k = 0; k < pb->K; ++k) zs += noise(pb, k, t, i);
-            double zbar = zs / (double)pb->K;
+            double zbar = zsum[j] / (double)pb->K;
             double g = h[j] * (xbar[j] - xs[j]) + pb->sigma * zbar;
             double d = g + pb->weight_decay * xbar[j];
             vbar[j] = pb->momentum * vbar[j] + d;
             xbar[j] = xbar[j] - gamma * vbar[j];
         }
     }
+    free(zsum);
 }
 
 int orc_num_threads(void)

@@ -1,0 +1,117 @@
+"""ADPSGD hot path on MI355X: Python side of the C ABI in ``include/adpsgd.h``.
+
+``_native`` holds the ctypes binding (functions named as in C).  ``Adpsgd``
+below owns one context together with its torch-allocated device buffers;
+torch supplies only device memory and the HIP stream.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+
+from ._native import (  # noqa: F401
+    AdpsgdError, EDEVICE, EINVAL, ENONFINITE, ESTATE, EXPORTED, LIB_PATH, LR_CONST, LR_COSINE,
+    LR_STEP, OK, PERIOD_ADAPTIVE, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
+    adpsgd_get_state, adpsgd_get_timing, adpsgd_hparams, adpsgd_init, adpsgd_last_error,
+    adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,
+    adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_schedule, adpsgd_set_state, adpsgd_set_timing,
+    adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
+    make_hparams,
+)
+
+
+def hparams_of(w) -> adpsgd_hparams:
+    """hparams from any object with the fields of the C struct (e.g. a workload)."""
+    return make_hparams(seed=w.seed, sigma=w.sigma, momentum=w.momentum, weight_decay=w.weight_decay,
+                        h_lo=w.h_lo, h_hi=w.h_hi, lr_kind=w.lr_kind, lr0=w.lr0,
+                        total_steps=w.total_steps, period_mode=w.period_mode, p_init=w.p_init,
+                        k_s=w.k_s, thr_lo=w.thr_lo, thr_hi=w.thr_hi)
+
+
+class Adpsgd:
+    """One ADPSGD context with its device buffers on a torch device.
+
+    x, m: float32 [K, P]; h, xstar: float32 [P]; workspace: uint8 sized by
+    adpsgd_workspace_bytes.  The stream is the torch stream current at
+    construction (or the one passed in).
+    """
+
+    def __init__(self, K: int, offsets, hp: adpsgd_hparams, device="cuda", stream=None):
+        import torch
+        self.torch = torch
+        off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+        self.K, self.P, self.T = int(K), int(off[-1]), len(off) - 1
+        self.offsets = off
+        self.hp = hp
+        self.device = torch.device(device)
+        if self.device.type != "cuda":
+            raise ValueError("the ADPSGD library runs on a GPU device only")
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        nbytes = adpsgd_workspace_bytes(self.K, self.P, off)
+        if nbytes == 0:
+            raise ValueError("invalid K, P or tensor offsets")
+        alloc = dict(device=self.device, dtype=torch.float32)
+        self.x = torch.empty((self.K, self.P), **alloc)
+        self.m = torch.empty((self.K, self.P), **alloc)
+        self.h = torch.empty((self.P,), **alloc)
+        self.xstar = torch.empty((self.P,), **alloc)
+        self.workspace = torch.empty((nbytes,), device=self.device, dtype=torch.uint8)
+        self.buf = adpsgd_buffers(x=self.x.data_ptr(), m=self.m.data_ptr(), h=self.h.data_ptr(),
+                                  xstar=self.xstar.data_ptr(), workspace=self.workspace.data_ptr(),
+                                  workspace_bytes=nbytes, stream=self.stream.cuda_stream)
+        with torch.cuda.device(self.device):
+            self.ctx = adpsgd_init(self.K, self.P, off, hp, self.buf)
+
+    @classmethod
+    def from_workload(cls, w, device="cuda", stream=None) -> "Adpsgd":
+        return cls(w.K, w.offsets(), hparams_of(w), device=device, stream=stream)
+
+    # -- the hot path
+    def local_steps(self, n: int) -> None:
+        adpsgd_local_steps(self.ctx, n)
+
+    def average(self) -> np.ndarray:
+        return adpsgd_average(self.ctx, self.T)
+
+    def step_average(self) -> np.ndarray:
+        return adpsgd_step_average(self.ctx, self.T)
+
+    def schedule(self, var: np.ndarray) -> int:
+        return adpsgd_schedule(self.ctx, var)
+
+    def run(self, n_steps: int, log_cap: Optional[int] = None, with_var: bool = True):
+        return adpsgd_run(self.ctx, n_steps, self.T, log_cap=log_cap, with_var=with_var)
+
+    def reset(self) -> None:
+        adpsgd_reset(self.ctx)
+
+    # -- state, timing
+    def get_state(self) -> adpsgd_state:
+        return adpsgd_get_state(self.ctx)
+
+    def set_state(self, st: adpsgd_state) -> None:
+        adpsgd_set_state(self.ctx, st)
+
+    def set_timing(self, on: bool) -> None:
+        adpsgd_set_timing(self.ctx, on)
+
+    def get_timing(self) -> adpsgd_timing:
+        return adpsgd_get_timing(self.ctx)
+
+    def close(self) -> None:
+        if getattr(self, "ctx", None):
+            adpsgd_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

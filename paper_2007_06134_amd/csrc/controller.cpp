@@ -1,0 +1,90 @@
+// Host-only parts of ADPSGD: the learning-rate schedules and the adaptive
+// period controller (Algorithm 2, lines 1-3 and 13-19).  No HIP here, so the
+// controller runs and is tested without a GPU.
+#include <climits>
+#include <cmath>
+#include <limits>
+
+#include "adpsgd.h"
+#include "common.hpp"
+
+namespace adpsgd {
+
+bool hparams_valid(const adpsgd_hparams *hp, std::string *why) {
+    auto bad = [&](const char *m) { if (why) *why = m; return false; };
+    if (!hp) return bad("hparams is NULL");
+    if (!(std::isfinite(hp->sigma) && hp->sigma >= 0)) return bad("sigma must be finite and >= 0");
+    if (!(hp->momentum >= 0 && hp->momentum < 1)) return bad("momentum must be in [0, 1)");
+    if (!(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0)) return bad("weight_decay must be finite and >= 0");
+    if (!(hp->h_lo > 0 && hp->h_lo <= hp->h_hi && std::isfinite(hp->h_hi))) return bad("need 0 < h_lo <= h_hi < inf");
+    if (hp->lr_kind < ADPSGD_LR_CONST || hp->lr_kind > ADPSGD_LR_COSINE) return bad("unknown lr_kind");
+    if (hp->period_mode != ADPSGD_PERIOD_CONST && hp->period_mode != ADPSGD_PERIOD_ADAPTIVE)
+        return bad("unknown period_mode");
+    if (!(std::isfinite(hp->lr0) && hp->lr0 > 0)) return bad("lr0 must be finite and > 0");
+    if (hp->total_steps < 1) return bad("total_steps must be >= 1");
+    if (hp->p_init < 1) return bad("p_init must be >= 1");
+    if (hp->p_max < 0 || (hp->p_max > 0 && hp->p_max < hp->p_init)) return bad("need p_max == 0 or p_max >= p_init");
+    if (hp->k_s < 0) return bad("k_s must be >= 0");
+    if (!(std::isfinite(hp->thr_lo) && std::isfinite(hp->thr_hi) && hp->thr_lo > 0 && hp->thr_lo <= hp->thr_hi))
+        return bad("need 0 < thr_lo <= thr_hi");
+    return true;
+}
+
+int32_t p_max_of(const adpsgd_hparams *hp) { return hp->p_max > 0 ? hp->p_max : INT32_MAX; }
+
+}  // namespace adpsgd
+
+using namespace adpsgd;
+
+extern "C" double adpsgd_lr(const adpsgd_hparams *hp, int64_t t) {
+    if (!hp) return std::numeric_limits<double>::quiet_NaN();
+    switch (hp->lr_kind) {
+    case ADPSGD_LR_STEP: {
+        // two 10x decays, at the half and three-quarter points of the schedule
+        const int n_decays = (t >= hp->total_steps / 2) + (t >= (3 * hp->total_steps) / 4);
+        double g = hp->lr0;
+        for (int d = 0; d < n_decays; ++d) g *= 0.1;
+        return g;
+    }
+    case ADPSGD_LR_COSINE:
+        return 0.5 * hp->lr0 * (1.0 + std::cos(M_PI * (double)t / (double)hp->total_steps));
+    default:
+        return hp->lr0;
+    }
+}
+
+extern "C" int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st) {
+    std::string why;
+    if (!st) return fail(ADPSGD_EINVAL, "state is NULL");
+    if (!hparams_valid(hp, &why)) return fail(ADPSGD_EINVAL, why);
+    *st = adpsgd_state{};
+    st->p = hp->p_init;
+    return ok();
+}
+
+extern "C" int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
+                                    double *margin) {
+    if (!hp || !st) return fail(ADPSGD_EINVAL, "NULL hparams or state");
+    if (margin) *margin = std::numeric_limits<double>::quiet_NaN();
+    if (!std::isfinite(S)) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
+    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE) return ok();
+    const double gamma = adpsgd_lr(hp, t);
+    if (t < hp->k_s) {
+        // sampling phase: C2 is the running (cumulative) mean of S / gamma
+        st->nC2 += 1;
+        st->C2 += (S / gamma - st->C2) / (double)st->nC2;
+        return ok();
+    }
+    const double lo = hp->thr_lo * gamma * st->C2;
+    const double hi = hp->thr_hi * gamma * st->C2;
+    if (margin && lo > 0) {
+        const double m_lo = S / lo - 1.0, m_hi = S / hi - 1.0;
+        *margin = std::fabs(m_lo) < std::fabs(m_hi) ? m_lo : m_hi;
+    }
+    if (S < lo) {
+        if (st->p < p_max_of(hp)) st->p += 1;
+    } else if (S > hi) {
+        if (st->p > 1) st->p -= 1;
+    }
+    return ok();
+}

@@ -1,0 +1,548 @@
+// Host runtime and C ABI of the ADPSGD hot path: argument validation, the tile
+// table of the segmented variance reduction, kernel launches on the caller's
+// stream, the pipelined Algorithm 2 driver, checkpoint state and timing.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <deque>
+#include <limits>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "adpsgd.h"
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace adpsgd {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string &msg) {
+    g_last_error = msg;
+    return code;
+}
+int ok() {
+    g_last_error.clear();
+    return ADPSGD_OK;
+}
+
+namespace {
+
+constexpr int kRing = 32;          // syncs whose variances may be in flight at once
+constexpr int kTimedMax = 1024;    // pending timed launches before a harvest
+constexpr int64_t kMaxK = 65536;
+constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
+
+enum TimedKind { kStep = 0, kFused = 1, kAverage = 2, kSegsum = 3 };
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool shape_valid(int32_t K, int64_t P, int32_t T, const int64_t *off, std::string *why) {
+    auto bad = [&](const std::string &m) { if (why) *why = m; return false; };
+    if (K < 1 || K > kMaxK) return bad("K must be in [1, 65536]");
+    if (P < 0) return bad("P must be >= 0");
+    if ((P + 3) / 4 > kMaxCounter) return bad("P/4 must be below 2^32");
+    if (T < 1 || T > (1 << 24)) return bad("T must be in [1, 2^24]");
+    if (!off) return bad("tensor_offsets is NULL");
+    if (off[0] != 0) return bad("tensor_offsets[0] must be 0");
+    for (int32_t i = 0; i < T; ++i)
+        if (off[i + 1] < off[i]) return bad("tensor_offsets must be non-decreasing");
+    if (off[T] != P) return bad("tensor_offsets[T] must equal P");
+    return true;
+}
+
+// Tiles: each tensor [a, b) is cut at multiples of kTileElems, so interior
+// tile boundaries are float4-aligned and no tile crosses a tensor boundary.
+void build_tiles(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::vector<int32_t> *begin) {
+    tiles->clear();
+    begin->assign(T + 1, 0);
+    for (int32_t tau = 0; tau < T; ++tau) {
+        (*begin)[tau] = (int32_t)tiles->size();
+        for (int64_t s = off[tau]; s < off[tau + 1];) {
+            const int64_t e = std::min(off[tau + 1], (s / kTileElems + 1) * kTileElems);
+            tiles->push_back(Tile{s, (int32_t)(e - s), tau});
+            s = e;
+        }
+    }
+    (*begin)[T] = (int32_t)tiles->size();
+}
+
+int64_t count_tiles(int32_t T, const int64_t *off) {
+    int64_t n = 0;
+    for (int32_t tau = 0; tau < T; ++tau)
+        for (int64_t s = off[tau]; s < off[tau + 1]; s = std::min(off[tau + 1], (s / kTileElems + 1) * kTileElems))
+            ++n;
+    return n;
+}
+
+struct Layout {
+    size_t tiles, tile_begin, partials, var, total;
+};
+
+Layout layout_for(int64_t n_tiles, int32_t T) {
+    Layout l;
+    l.tiles = 0;
+    l.tile_begin = align_up(l.tiles + sizeof(Tile) * (size_t)std::max<int64_t>(n_tiles, 1), 256);
+    l.partials = align_up(l.tile_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
+    l.var = align_up(l.partials + sizeof(double) * (size_t)std::max<int64_t>(n_tiles, 1), 256);
+    l.total = align_up(l.var + sizeof(double) * (size_t)kRing * (size_t)T, 256);
+    return l;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(ADPSGD_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr)                                         \
+    do {                                                      \
+        hipError_t e_ = (expr);                               \
+        if (e_ != hipSuccess) return hip_fail(e_, #expr);     \
+    } while (0)
+
+struct TimedLaunch {
+    int kind;
+    hipEvent_t start, stop;
+};
+
+}  // namespace
+}  // namespace adpsgd
+
+using namespace adpsgd;
+
+struct adpsgd_ctx {
+    int32_t K = 0;
+    int64_t P = 0;
+    int32_t T = 0;
+    std::vector<int64_t> offsets;
+    std::vector<Tile> tiles;
+    std::vector<int32_t> tile_begin;
+    adpsgd_hparams hp{};
+    adpsgd_buffers buf{};
+    hipStream_t stream = nullptr;
+    int device = 0;
+    Tile *d_tiles = nullptr;
+    int32_t *d_tile_begin = nullptr;
+    double *d_partials = nullptr;
+    double *d_var = nullptr;        // [kRing][T] device
+    double *h_var = nullptr;        // [kRing][T] pinned host
+    hipEvent_t ring_ev[kRing] = {};
+    adpsgd_state st{};
+    bool vec = true;                // P % 4 == 0: dwordx4 rows
+    bool nontemporal = false;
+    RoundKeys rk{};
+    bool timing = false;
+    std::deque<TimedLaunch> timed;
+    std::vector<hipEvent_t> ev_pool;
+    double t_ms[4] = {0, 0, 0, 0};
+    int64_t t_n[4] = {0, 0, 0, 0};
+};
+
+namespace {
+
+void release(adpsgd_ctx *c) {
+    if (!c) return;
+    for (auto &ev : c->ring_ev)
+        if (ev) (void)hipEventDestroy(ev);
+    for (auto &tl : c->timed) {
+        (void)hipEventDestroy(tl.start);
+        (void)hipEventDestroy(tl.stop);
+    }
+    for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
+    if (c->h_var) (void)hipHostFree(c->h_var);
+    delete c;
+}
+
+int pool_event(adpsgd_ctx *c, hipEvent_t *ev) {
+    if (!c->ev_pool.empty()) {
+        *ev = c->ev_pool.back();
+        c->ev_pool.pop_back();
+        return ok();
+    }
+    HIP_TRY(hipEventCreate(ev));
+    return ok();
+}
+
+// Fold finished timed launches into the totals (all of them if wait_all).
+int harvest(adpsgd_ctx *c, bool wait_all) {
+    while (!c->timed.empty()) {
+        TimedLaunch tl = c->timed.front();
+        if (wait_all) {
+            HIP_TRY(hipEventSynchronize(tl.stop));
+        } else {
+            hipError_t q = hipEventQuery(tl.stop);
+            if (q == hipErrorNotReady) break;
+            if (q != hipSuccess) return hip_fail(q, "hipEventQuery");
+        }
+        float ms = 0.f;
+        HIP_TRY(hipEventElapsedTime(&ms, tl.start, tl.stop));
+        c->t_ms[tl.kind] += ms;
+        c->t_n[tl.kind] += 1;
+        c->ev_pool.push_back(tl.start);
+        c->ev_pool.push_back(tl.stop);
+        c->timed.pop_front();
+    }
+    return ok();
+}
+
+template <class F>
+int timed_launch(adpsgd_ctx *c, int kind, F launch) {
+    if (!c->timing) {
+        HIP_TRY(launch());
+        return ok();
+    }
+    if ((int)c->timed.size() >= kTimedMax) {
+        int rc = harvest(c, false);
+        if (rc) return rc;
+        if ((int)c->timed.size() >= kTimedMax) {
+            rc = harvest(c, true);
+            if (rc) return rc;
+        }
+    }
+    TimedLaunch tl{kind, nullptr, nullptr};
+    int rc = pool_event(c, &tl.start);
+    if (rc) return rc;
+    rc = pool_event(c, &tl.stop);
+    if (rc) return rc;
+    HIP_TRY(hipEventRecord(tl.start, c->stream));
+    HIP_TRY(launch());
+    HIP_TRY(hipEventRecord(tl.stop, c->stream));
+    c->timed.push_back(tl);
+    return ok();
+}
+
+StepParams step_params(const adpsgd_ctx *c, int64_t t) {
+    StepParams p;
+    p.x = c->buf.x;
+    p.m = c->buf.m;
+    p.h = c->buf.h;
+    p.xs = c->buf.xstar;
+    p.P = c->P;
+    p.n_groups = (c->P + 3) / 4;
+    p.K = c->K;
+    p.t = (uint32_t)t;
+    p.sigma = (float)c->hp.sigma;
+    p.mu = (float)c->hp.momentum;
+    p.wd = (float)c->hp.weight_decay;
+    p.gamma = (float)adpsgd_lr(&c->hp, t);
+    p.rk = c->rk;
+    return p;
+}
+
+int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
+    for (int64_t j = 0; j < n; ++j) {
+        const StepParams p = step_params(c, t0 + j);
+        int rc = timed_launch(c, kStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->stream); });
+        if (rc) return rc;
+    }
+    return ok();
+}
+
+// Sync (fused behind step t if fused) with its variances landing in ring slot.
+int enqueue_sync(adpsgd_ctx *c, bool fused, int64_t t, int slot) {
+    SyncParams sp;
+    sp.s = step_params(c, t);
+    sp.tiles = c->d_tiles;
+    sp.partials = c->d_partials;
+    const int64_t n_tiles = (int64_t)c->tiles.size();
+    int rc = timed_launch(c, fused ? kFused : kAverage, [&] {
+        return launch_tile_sync(sp, n_tiles, fused, c->vec, c->nontemporal, c->stream);
+    });
+    if (rc) return rc;
+    double *dv = c->d_var + (size_t)slot * c->T;
+    rc = timed_launch(c, kSegsum, [&] {
+        return launch_segsum(c->d_tile_begin, c->d_partials, dv, c->T, c->K, c->stream);
+    });
+    if (rc) return rc;
+    HIP_TRY(hipMemcpyAsync(c->h_var + (size_t)slot * c->T, dv, sizeof(double) * c->T, hipMemcpyDeviceToHost,
+                           c->stream));
+    HIP_TRY(hipEventRecord(c->ring_ev[slot], c->stream));
+    return ok();
+}
+
+double sum_var(const double *v, int32_t T) {
+    double s = 0.0;
+    for (int32_t i = 0; i < T; ++i) s += v[i];
+    return s;
+}
+
+int check_ctx(const adpsgd_ctx *c) {
+    if (!c) return fail(ADPSGD_EINVAL, "context is NULL");
+    return ok();
+}
+
+}  // namespace
+
+extern "C" const char *adpsgd_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const int64_t *offsets) {
+    std::string why;
+    if (!shape_valid(K, P, T, offsets, &why)) return 0;
+    return layout_for(count_tiles(T, offsets), T).total;
+}
+
+extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t T, const adpsgd_hparams *hp,
+                           const adpsgd_buffers *buf, adpsgd_ctx **out) {
+    std::string why;
+    if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!shape_valid(K, P, T, offsets, &why)) return fail(ADPSGD_EINVAL, why);
+    if (!hparams_valid(hp, &why)) return fail(ADPSGD_EINVAL, why);
+    if (!buf) return fail(ADPSGD_EINVAL, "buffers is NULL");
+    if (P > 0 && (!buf->x || !buf->m || !buf->h || !buf->xstar))
+        return fail(ADPSGD_EINVAL, "x, m, h and xstar must be non-NULL");
+    if (!aligned(buf->x, 16) || !aligned(buf->m, 16) || !aligned(buf->h, 16) || !aligned(buf->xstar, 16))
+        return fail(ADPSGD_EINVAL, "x, m, h and xstar must be 16-byte aligned");
+    const int64_t n_tiles = count_tiles(T, offsets);
+    if (n_tiles >= (int64_t(1) << 31)) return fail(ADPSGD_EINVAL, "too many tiles");
+    const Layout lay = layout_for(n_tiles, T);
+    if (!buf->workspace || !aligned(buf->workspace, 256)) return fail(ADPSGD_EINVAL, "workspace must be 256-byte aligned");
+    if (buf->workspace_bytes < lay.total)
+        return fail(ADPSGD_EINVAL, "workspace too small: need " + std::to_string(lay.total) + " bytes");
+
+    adpsgd_ctx *c = new (std::nothrow) adpsgd_ctx();
+    if (!c) return fail(ADPSGD_EINVAL, "out of host memory");
+    c->K = K;
+    c->P = P;
+    c->T = T;
+    c->offsets.assign(offsets, offsets + T + 1);
+    build_tiles(T, offsets, &c->tiles, &c->tile_begin);
+    c->hp = *hp;
+    c->buf = *buf;
+    c->stream = (hipStream_t)buf->stream;
+    c->vec = (P % 4) == 0;
+    c->rk = round_keys(hp->seed);
+    char *ws = (char *)buf->workspace;
+    c->d_tiles = (Tile *)(ws + lay.tiles);
+    c->d_tile_begin = (int32_t *)(ws + lay.tile_begin);
+    c->d_partials = (double *)(ws + lay.partials);
+    c->d_var = (double *)(ws + lay.var);
+
+    auto bail = [&](hipError_t e, const char *what) {
+        int rc = hip_fail(e, what);
+        std::string msg = g_last_error;
+        release(c);
+        g_last_error = msg;
+        return rc;
+    };
+    hipError_t e;
+    if ((e = hipGetDevice(&c->device)) != hipSuccess) return bail(e, "hipGetDevice");
+    if ((e = hipHostMalloc((void **)&c->h_var, sizeof(double) * kRing * (size_t)T, hipHostMallocDefault)) != hipSuccess)
+        return bail(e, "hipHostMalloc");
+    for (auto &ev : c->ring_ev)
+        if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail(e, "hipEventCreate");
+    if (!c->tiles.empty() &&
+        (e = hipMemcpyAsync(c->d_tiles, c->tiles.data(), sizeof(Tile) * c->tiles.size(), hipMemcpyHostToDevice,
+                            c->stream)) != hipSuccess)
+        return bail(e, "copy tile table");
+    if ((e = hipMemcpyAsync(c->d_tile_begin, c->tile_begin.data(), sizeof(int32_t) * (T + 1), hipMemcpyHostToDevice,
+                            c->stream)) != hipSuccess)
+        return bail(e, "copy tile offsets");
+    if ((e = hipMemsetAsync(c->d_var, 0, sizeof(double) * kRing * (size_t)T, c->stream)) != hipSuccess)
+        return bail(e, "clear variance ring");
+    if (P > 0) {
+        if ((e = launch_init_problem(buf->h, buf->xstar, P, hp->seed, hp->h_lo, hp->h_hi, c->stream)) != hipSuccess)
+            return bail(e, "init_problem launch");
+        const size_t bytes = sizeof(float) * (size_t)K * (size_t)P;
+        if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
+        if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
+    }
+    if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e, "hipStreamSynchronize");
+    c->st = adpsgd_state{};
+    c->st.p = hp->p_init;
+    *out = c;
+    return ok();
+}
+
+extern "C" int adpsgd_reset(adpsgd_ctx *c) {
+    if (int rc = check_ctx(c)) return rc;
+    if (c->P > 0) {
+        const size_t bytes = sizeof(float) * (size_t)c->K * (size_t)c->P;
+        HIP_TRY(hipMemsetAsync(c->buf.x, 0, bytes, c->stream));
+        HIP_TRY(hipMemsetAsync(c->buf.m, 0, bytes, c->stream));
+    }
+    c->st = adpsgd_state{};
+    c->st.p = c->hp.p_init;
+    return ok();
+}
+
+extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
+    if (int rc = check_ctx(c)) return rc;
+    if (n < 0) return fail(ADPSGD_EINVAL, "n must be >= 0");
+    if (c->st.t + n > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
+    if (int rc = enqueue_steps(c, c->st.t, n)) return rc;
+    c->st.t += n;
+    c->st.cnt += n;
+    return ok();
+}
+
+static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!var_out) return fail(ADPSGD_EINVAL, "var_out is NULL");
+    if (fused && c->st.t + 1 > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
+    if (int rc = enqueue_sync(c, fused, c->st.t, 0)) return rc;
+    HIP_TRY(hipEventSynchronize(c->ring_ev[0]));
+    std::memcpy(var_out, c->h_var, sizeof(double) * c->T);
+    if (fused) c->st.t += 1;
+    c->st.cnt = 0;
+    return ok();
+}
+
+extern "C" int adpsgd_average(adpsgd_ctx *c, double *var_out) { return sync_now(c, false, var_out); }
+
+extern "C" int adpsgd_step_average(adpsgd_ctx *c, double *var_out) { return sync_now(c, true, var_out); }
+
+extern "C" int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_period) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!var) return fail(ADPSGD_EINVAL, "var is NULL");
+    if (c->st.t < 1) return fail(ADPSGD_ESTATE, "no step has been taken yet");
+    int rc = adpsgd_sched_on_sync(&c->hp, &c->st, c->st.t - 1, sum_var(var, c->T), nullptr);
+    if (next_period) *next_period = c->st.p;
+    return rc;
+}
+
+extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
+                          int64_t *n_syncs) {
+    if (int rc = check_ctx(c)) return rc;
+    if (n_steps < 0 || log_cap < 0) return fail(ADPSGD_EINVAL, "n_steps and log_cap must be >= 0");
+    if (log_cap > 0 && !log) return fail(ADPSGD_EINVAL, "log is NULL with log_cap > 0");
+    if (c->st.t + n_steps > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
+
+    const adpsgd_hparams &hp = c->hp;
+    const bool adaptive = hp.period_mode == ADPSGD_PERIOD_ADAPTIVE;
+    const int64_t end = c->st.t + n_steps;
+    // Enqueue side: t_enq/cnt_enq track what is on the stream.  c->st (p, C2)
+    // is the controller's view, advanced as syncs are read back in order.
+    int64_t t_enq = c->st.t, cnt_enq = c->st.cnt;
+    int32_t p_known = c->st.p;
+    struct Pending { int64_t t; int32_t p; int slot; bool decisive; };
+    std::deque<Pending> pend;
+    int64_t n_enq_syncs = 0, n_done = 0;
+    bool blocked = false;   // a sync whose decision sets the next period is in flight
+    int status = ADPSGD_OK;
+
+    while (true) {
+        while (status == ADPSGD_OK && !blocked && t_enq < end && (int)pend.size() < kRing) {
+            const int64_t to_sync = std::max<int64_t>(p_known - cnt_enq, 1);
+            if (t_enq + to_sync > end) {   // the run ends inside this period
+                if ((status = enqueue_steps(c, t_enq, end - t_enq))) break;
+                cnt_enq += end - t_enq;
+                t_enq = end;
+                break;
+            }
+            if ((status = enqueue_steps(c, t_enq, to_sync - 1))) break;
+            t_enq += to_sync - 1;
+            const int slot = (int)(n_enq_syncs % kRing);
+            if ((status = enqueue_sync(c, true, t_enq, slot))) break;
+            const bool decisive = adaptive && t_enq >= hp.k_s;
+            pend.push_back(Pending{t_enq, p_known, slot, decisive});
+            ++n_enq_syncs;
+            t_enq += 1;
+            cnt_enq = 0;
+            if (decisive) {
+                // p moves by at most one, so the next period has at least
+                // max(p-1, 1) steps; run those while the variance is read back
+                const int64_t pre = std::min<int64_t>(std::max(p_known - 1, 1) - 1, end - t_enq);
+                if ((status = enqueue_steps(c, t_enq, pre))) break;
+                t_enq += pre;
+                cnt_enq = pre;
+                blocked = true;
+            }
+        }
+        if (pend.empty() || status != ADPSGD_OK) break;
+        const Pending q = pend.front();
+        pend.pop_front();
+        hipError_t e = hipEventSynchronize(c->ring_ev[q.slot]);
+        if (e != hipSuccess) { status = hip_fail(e, "wait for variance"); break; }
+        const double *var = c->h_var + (size_t)q.slot * c->T;
+        const double S = sum_var(var, c->T);
+        double margin = std::numeric_limits<double>::quiet_NaN();
+        const int rc = adpsgd_sched_on_sync(&hp, &c->st, q.t, S, &margin);
+        if (n_done < log_cap) {
+            log[n_done] = adpsgd_sync_rec{q.t, q.p, 0, S, c->st.C2, adpsgd_lr(&hp, q.t), margin};
+            if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
+        }
+        ++n_done;
+        if (rc) { status = rc; break; }
+        if (q.decisive) {
+            p_known = c->st.p;
+            blocked = false;
+        }
+        if (c->timing) {
+            int hr = harvest(c, false);
+            if (hr) { status = hr; break; }
+        }
+    }
+    // whatever was enqueued runs to completion; the state reflects it
+    hipError_t e = hipStreamSynchronize(c->stream);
+    c->st.t = t_enq;
+    c->st.cnt = cnt_enq;
+    if (n_syncs) *n_syncs = n_done;
+    if (status != ADPSGD_OK) return status;
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    return ok();
+}
+
+extern "C" int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
+    *out = c->st;
+    return ok();
+}
+
+extern "C" int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!in) return fail(ADPSGD_EINVAL, "state is NULL");
+    if (in->t < 0 || in->t >= kMaxCounter || in->cnt < 0 || in->nC2 < 0 || in->p < 1 || in->p > p_max_of(&c->hp) ||
+        !std::isfinite(in->C2))
+        return fail(ADPSGD_EINVAL, "invalid state");
+    c->st = *in;
+    return ok();
+}
+
+extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t on) {
+    if (int rc = check_ctx(c)) return rc;
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (int rc = harvest(c, true)) return rc;
+    c->timing = on != 0;
+    for (int i = 0; i < 4; ++i) { c->t_ms[i] = 0.0; c->t_n[i] = 0; }
+    return ok();
+}
+
+extern "C" int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
+    HIP_TRY(hipStreamSynchronize(c->stream));
+    if (int rc = harvest(c, true)) return rc;
+    *out = adpsgd_timing{c->t_ms[kStep], c->t_n[kStep], c->t_ms[kFused], c->t_n[kFused],
+                         c->t_ms[kAverage], c->t_n[kAverage], c->t_ms[kSegsum], c->t_n[kSegsum]};
+    return ok();
+}
+
+extern "C" int adpsgd_destroy(adpsgd_ctx *c) {
+    if (!c) return ok();
+    hipError_t e = hipStreamSynchronize(c->stream);
+    release(c);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    return ok();
+}
+
+extern "C" int adpsgd_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0, int64_t n_groups,
+                                  uint32_t *dev_out, void *stream) {
+    if (n_groups < 0 || g0 < 0 || g0 + n_groups > kMaxCounter) return fail(ADPSGD_EINVAL, "bad group range");
+    if (n_groups > 0 && (!dev_out || !aligned(dev_out, 16))) return fail(ADPSGD_EINVAL, "dev_out must be 16-byte aligned");
+    HIP_TRY(launch_philox_dump(seed, c1, c2, c3, g0, n_groups, dev_out, (hipStream_t)stream));
+    return ok();
+}
+
+extern "C" int adpsgd_normal_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0, int64_t n_groups,
+                                  float *dev_out, void *stream) {
+    if (n_groups < 0 || g0 < 0 || g0 + n_groups > kMaxCounter) return fail(ADPSGD_EINVAL, "bad group range");
+    if (n_groups > 0 && (!dev_out || !aligned(dev_out, 16))) return fail(ADPSGD_EINVAL, "dev_out must be 16-byte aligned");
+    HIP_TRY(launch_normal_dump(seed, c1, c2, c3, g0, n_groups, dev_out, (hipStream_t)stream));
+    return ok();
+}

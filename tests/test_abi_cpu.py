@@ -1,0 +1,198 @@
+"""The C ABI without a GPU: exported symbols, argument validation and the host
+controller, checked against the oracle's independent implementation."""
+import ctypes as C
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def A():
+    import paper_2007_06134_amd as A
+    return A
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "adpsgd.h")).read()
+    return sorted(set(re.findall(r"ADPSGD_API[^;(]*?\b(adpsgd_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol(A):
+    names = _declared()
+    assert len(names) >= 19
+    lib = C.CDLL(A.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(A.EXPORTED)
+
+
+def test_library_exports_nothing_else(A):
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", A.LIB_PATH], capture_output=True, text=True).stdout
+    syms = [ln.split()[-1] for ln in out.splitlines() if ln.split() and ln.split()[-2] == "T"]
+    assert sorted(s for s in syms if s.startswith("adpsgd_")) == _declared()
+
+
+def _hp(A, **kw):
+    w = W.full_workloads()["resnet50_like"].replace(**kw)
+    return A.hparams_of(w), w
+
+
+@pytest.mark.parametrize("key", ["quad_small", "resnet18_like", "resnet50_like", "vgg16_const8"])
+def test_learning_rate_matches_oracle(A, key):
+    w = W.full_workloads()[key]
+    hp = A.hparams_of(w)
+    o = oracle.Oracle(w)
+    for t in range(0, w.total_steps, max(1, w.total_steps // 97)):
+        assert A.adpsgd_lr(hp, t) == pytest.approx(o.lr(t), rel=1e-14)
+    for t in (w.total_steps // 2 - 1, w.total_steps // 2, 3 * w.total_steps // 4 - 1, 3 * w.total_steps // 4):
+        assert A.adpsgd_lr(hp, t) == pytest.approx(o.lr(t), rel=1e-14)
+
+
+def _lib_trace(A, w, S_fn):
+    hp = A.hparams_of(w)
+    st = A.adpsgd_sched_init(hp)
+    out = []
+    for t in range(w.total_steps):
+        st.cnt += 1
+        if st.cnt == st.p:
+            st.cnt = 0
+            p_used = st.p
+            A.adpsgd_sched_on_sync(hp, st, t, S_fn(t, A.adpsgd_lr(hp, t)))
+            out.append((t, p_used))
+    return out, st
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_controller_matches_oracle_on_random_variances(A, seed):
+    w = W.full_workloads()["resnet18_like"].replace(total_steps=3000, k_s=600, p_init=3)
+    rng = np.random.default_rng(seed)
+    noise = rng.lognormal(0.0, 0.35, size=4000)
+    # S drifts with gamma and with the period, like the variance at a sync does
+    S_fn = lambda t, g: float(noise[t] * g * (0.9 + 0.3 * math.sin(t / 300.0)))
+    lib, st_l = _lib_trace(A, w, S_fn)
+    orc, st_o = oracle.controller_trace(w, S_fn)
+    assert lib == orc
+    assert st_l.p == st_o.p and st_l.nC2 == st_o.nC2
+    assert st_l.C2 == pytest.approx(st_o.C2, rel=1e-12)
+    assert len({p for _, p in lib}) > 3
+
+
+def test_controller_scripted_cases(A):
+    w = W.full_workloads()["resnet50_like"].replace(total_steps=400, k_s=100, p_init=4,
+                                                    lr_kind=W.LR_CONST)
+    # zero variance after sampling: p grows by one each sync
+    trace, _ = _lib_trace(A, w, lambda t, g: (g if t < 100 else 0.0))
+    after = [p for t, p in trace if t >= 100]
+    assert after[:5] == [4, 5, 6, 7, 8]
+    # huge variance: p clamps at 1
+    trace, st = _lib_trace(A, w, lambda t, g: (g if t < 100 else 1e30))
+    assert [p for t, p in trace if t >= 100][:5] == [4, 3, 2, 1, 1] and st.p == 1
+    # p_max bounds the growth
+    hp = A.hparams_of(w)
+    hp.p_max = 6
+    st = A.adpsgd_sched_init(hp)
+    st.C2 = 1.0
+    for _ in range(5):
+        A.adpsgd_sched_on_sync(hp, st, 200, 0.0)
+    assert st.p == 6
+
+
+def test_controller_margin_and_sampling(A):
+    hp, w = _hp(A, k_s=10, lr_kind=W.LR_CONST, lr0=0.1)
+    st = A.adpsgd_sched_init(hp)
+    for S in (1.0, 3.0):
+        m = A.adpsgd_sched_on_sync(hp, st, 5, S)
+        assert math.isnan(m)
+    assert st.C2 == pytest.approx(20.0) and st.nC2 == 2 and st.p == 4
+    m = A.adpsgd_sched_on_sync(hp, st, 50, 0.7 * 0.1 * 20.0 * 1.01)
+    assert m == pytest.approx(0.01, rel=1e-9) and st.p == 4
+
+
+def test_controller_non_finite_keeps_state(A):
+    hp, _ = _hp(A)
+    st = A.adpsgd_sched_init(hp)
+    st.p, st.C2, st.nC2 = 7, 2.0, 3
+    for bad in (float("nan"), float("inf"), -float("inf")):
+        with pytest.raises(A.AdpsgdError) as e:
+            A.adpsgd_sched_on_sync(hp, st, 500, bad)
+        assert e.value.code == A.ENONFINITE
+        assert (st.p, st.C2, st.nC2) == (7, 2.0, 3)
+
+
+def test_constant_mode_never_changes_period(A):
+    hp, _ = _hp(A, period_mode=W.PERIOD_CONST, p_init=8)
+    st = A.adpsgd_sched_init(hp)
+    for t, S in [(10, 0.0), (500, 1e9), (900, 1e-9)]:
+        A.adpsgd_sched_on_sync(hp, st, t, S)
+    assert st.p == 8 and st.C2 == 0.0
+
+
+@pytest.mark.parametrize("field,value", [
+    ("sigma", -1.0), ("momentum", 1.0), ("weight_decay", -1e-4), ("h_lo", 0.0), ("h_hi", 1e-9),
+    ("lr_kind", 7), ("period_mode", 3), ("lr0", 0.0), ("total_steps", 0), ("p_init", 0),
+    ("k_s", -1), ("thr_lo", 2.0), ("p_max", 2),
+])
+def test_invalid_hparams_rejected(A, field, value):
+    hp, _ = _hp(A)
+    setattr(hp, field, value)
+    with pytest.raises(A.AdpsgdError) as e:
+        A.adpsgd_sched_init(hp)
+    assert e.value.code == A.EINVAL and A.adpsgd_last_error()
+
+
+def _fake_buffers(A, ws=1 << 20, misalign=0):
+    # host addresses standing in for device pointers: validation reads no memory
+    arena = (C.c_char * (4096 + ws))()
+    base = (C.addressof(arena) + 255) // 256 * 256
+    b = A.adpsgd_buffers(x=base + misalign, m=base, h=base, xstar=base, workspace=base,
+                         workspace_bytes=ws, stream=None)
+    return b, arena
+
+
+@pytest.mark.parametrize("K,offsets", [
+    (0, [0, 8]), (70000, [0, 8]), (2, [1, 8]), (2, [0, 9, 8]), (2, [0, 4, 9]),
+])
+def test_init_rejects_bad_shapes(A, K, offsets):
+    hp, _ = _hp(A)
+    b, _arena = _fake_buffers(A)
+    with pytest.raises(A.AdpsgdError) as e:
+        A.adpsgd_init(K, 8, offsets, hp, b)
+    assert e.value.code == A.EINVAL
+    assert A.adpsgd_workspace_bytes(K, 8, offsets) == 0
+
+
+def test_init_rejects_bad_buffers(A):
+    hp, _ = _hp(A)
+    b, _arena = _fake_buffers(A, misalign=4)
+    with pytest.raises(A.AdpsgdError) as e:
+        A.adpsgd_init(2, 8, [0, 8], hp, b)
+    assert e.value.code == A.EINVAL and "aligned" in A.adpsgd_last_error()
+    need = A.adpsgd_workspace_bytes(2, 8, [0, 8])
+    b, _arena = _fake_buffers(A, ws=need - 1)
+    with pytest.raises(A.AdpsgdError) as e:
+        A.adpsgd_init(2, 8, [0, 8], hp, b)
+    assert e.value.code == A.EINVAL and "workspace" in A.adpsgd_last_error()
+
+
+def test_workspace_bytes_grows_with_tiles(A):
+    small = A.adpsgd_workspace_bytes(8, 4096, [0, 4096])
+    big = A.adpsgd_workspace_bytes(8, 4096 * 100, [0, 4096 * 100])
+    many = A.adpsgd_workspace_bytes(8, 4096, list(range(0, 4097, 16)))
+    assert 0 < small < big and small < many
+    assert A.adpsgd_workspace_bytes(4, 0, [0, 0, 0]) > 0   # empty tensors are allowed
+
+
+def test_null_context_and_dump_ranges(A):
+    assert A._native.lib.adpsgd_local_steps(None, 1) == A.EINVAL
+    assert A._native.lib.adpsgd_destroy(None) == A.OK
+    assert A._native.lib.adpsgd_philox_dump(0, 0, 0, 0, 2**32 - 4, 8, None, None) == A.EINVAL
+    assert A._native.lib.adpsgd_normal_dump(0, 0, 0, 0, -1, 8, None, None) == A.EINVAL

@@ -1,0 +1,112 @@
+"""Full-size runs on cuda:0, in the launch configuration the bench times.
+
+The oracle cannot replay a full run of 1e11-1e12 element updates, so these
+tests check, at full size, what it can compute one element at a time:
+
+* the replica mean at sampled elements.  Syncs preserve the mean of x and of
+  m, and the dynamics are affine, so the mean follows one momentum-SGD run on
+  the K-averaged noise whatever the sync schedule (adaptive runs included);
+* with a constant period the schedule is known in advance, so the oracle runs
+  the sampled elements exactly (every replica, x and m) and the full
+  per-tensor variance of every tensor it covers completely;
+* the controller's decisions, recomputed from the reported S values.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import max_rel_err, rel_err
+
+pytestmark = pytest.mark.gpu
+
+PARAM_TOL = 1e-4
+VAR_TOL = 1e-3
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _sample(w, whole_below=30_000, seed=0):
+    """Sorted element indices: whole small tensors, ends and random interior of the rest."""
+    rng = np.random.default_rng(seed)
+    off = w.offsets()
+    idx, whole = [], []
+    budget_whole = 0
+    ends = 8 if w.T <= 64 else 2
+    per_tensor = max(4, 2048 // w.T)
+    for tau in range(w.T):
+        lo, hi = int(off[tau]), int(off[tau + 1])
+        if hi - lo <= whole_below and budget_whole + (hi - lo) <= 4 * whole_below:
+            idx.append(np.arange(lo, hi)); whole.append(tau); budget_whole += hi - lo
+        else:
+            idx.append(np.arange(lo, lo + min(ends, hi - lo)))
+            idx.append(np.arange(max(lo, hi - ends), hi))
+            idx.append(rng.integers(lo, hi, size=min(per_tensor, hi - lo)))
+    idx = np.unique(np.concatenate(idx)).astype(np.int64)
+    return idx, whole
+
+
+def _check_controller(w, recs):
+    t, p, S, gamma = recs["t"], recs["p"], recs["S"], recs["gamma"]
+    assert len(t) > 0 and t[0] == w.p_init - 1 and p[0] == w.p_init
+    assert np.all(np.diff(t) == p[1:]), "each period must last p steps"
+    if w.period_mode == W.PERIOD_CONST:
+        assert np.all(p == w.p_init)
+        return
+    C2, n = 0.0, 0
+    for j in range(len(t) - 1):
+        if t[j] < w.k_s:
+            n += 1
+            C2 += (S[j] / gamma[j] - C2) / n
+            assert p[j + 1] == p[j]
+            assert recs["C2"][j] == pytest.approx(C2, rel=1e-12)
+        elif S[j] < w.thr_lo * gamma[j] * C2:
+            assert p[j + 1] == p[j] + 1
+        elif S[j] > w.thr_hi * gamma[j] * C2:
+            assert p[j + 1] == max(p[j] - 1, 1)
+        else:
+            assert p[j + 1] == p[j]
+
+
+@pytest.fixture(scope="module")
+def A():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2007_06134_amd as A
+    return A
+
+
+@pytest.mark.parametrize("key", list(W.full_workloads()))
+def test_full_size_run(A, key):
+    import torch
+    w = W.full_workloads()[key]
+    _say(f"full size {key}: K={w.K} P={w.P} T={w.T} N={w.total_steps}")
+    # whole tensors only where the oracle can replay them (constant period)
+    idx, whole = _sample(w, whole_below=30_000 if w.period_mode == W.PERIOD_CONST else 0)
+    it = torch.from_numpy(idx).cuda()
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, var, n = eng.run(w.total_steps)
+        xs_sel = eng.x.index_select(1, it).double().cpu().numpy()
+        ms_sel = eng.m.index_select(1, it).double().cpu().numpy()
+    _say(f"  {n} syncs, p {recs['p'].min()}..{recs['p'].max()}")
+    assert n == len(recs) and np.all(np.isfinite(recs["S"]))
+    np.testing.assert_allclose(var.sum(axis=1), recs["S"], rtol=1e-12)
+    _check_controller(w, recs)
+
+    o = oracle.Oracle(w)
+    xbar, vbar = o.mean_trajectory(w.total_steps, idx=idx)
+    sub_off = np.searchsorted(idx, w.offsets())
+    assert max_rel_err(xs_sel.mean(axis=0), xbar, sub_off) < PARAM_TOL
+    assert max_rel_err(ms_sel.mean(axis=0), vbar, sub_off) < PARAM_TOL
+
+    if w.period_mode == W.PERIOD_CONST:
+        r = o.run(idx=idx)
+        assert np.array_equal(recs["t"], r.sync_t)
+        assert max_rel_err(xs_sel, r.x, sub_off) < PARAM_TOL
+        assert max_rel_err(ms_sel, r.v, sub_off) < PARAM_TOL
+        for tau in whole:
+            assert rel_err(var[:, tau], r.var[:, tau]) < VAR_TOL, tau

@@ -1,0 +1,276 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, on cuda:0.
+
+Bars: Philox words bit-exact; fp32 parameters and momentum within 1e-4 max
+relative error (per tensor, against max(|oracle|, 1e-2 rms)); per-tensor
+variances within 1e-3 relative; the sequence of sync steps identical.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from helpers import gpu_run, max_rel_err, rel_err
+
+pytestmark = pytest.mark.gpu
+
+PARAM_TOL = 1e-4
+VAR_TOL = 1e-3
+
+
+def _say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def A():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2007_06134_amd as A
+    return A
+
+
+def _tiny(K=4, sizes=(4096,), **kw):
+    base = dict(name="tiny", K=K, sizes=tuple(sizes), seed=21, sigma=0.1, momentum=0.9,
+                weight_decay=5e-4, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.05,
+                total_steps=40, period_mode=W.PERIOD_CONST, p_init=10**6, k_s=0)
+    base.update(kw)
+    return W.Workload(**base)
+
+
+# ---------------------------------------------------------------- generator
+
+@pytest.mark.parametrize("seed,c,g0,n", [
+    (0, (0, 0, 0), 0, 4096), (1, (3, 17, 0), 12345, 1000),
+    ((7 << 32) | 99, (31, 4999, 1), 2**32 - 777, 777), (0xDEADBEEFCAFEBABE, (5, 6, 2), 1, 4096 * 3 + 5),
+])
+def test_philox_words_bit_exact(A, seed, c, g0, n):
+    import torch
+    _say(f"philox dump seed={seed} c={c} g0={g0} n={n}")
+    out = torch.zeros(4 * n, dtype=torch.int32, device="cuda")
+    A.adpsgd_philox_dump(seed, *c, g0, n, out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32).reshape(n, 4)
+    want = oracle.philox_groups(seed, *c, g0, n)
+    assert np.array_equal(got, want)
+
+
+def test_normals_match_oracle(A):
+    import torch
+    n = 1 << 18
+    _say("normal dump")
+    out = torch.zeros(4 * n, dtype=torch.float32, device="cuda")
+    A.adpsgd_normal_dump(77, 2, 9, 0, 0, n, out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    want = oracle.normals_groups(77, 2, 9, 0, 0, n)
+    err = np.abs(got - want) / np.maximum(1.0, np.abs(want))
+    # fp32 log/sqrt/sincospi against fp64: a few ulp of the result
+    assert err.max() < 2e-6, err.max()
+
+
+@pytest.mark.parametrize("P", [1, 5, 4096, 10_001])
+def test_problem_data_matches_oracle(A, P):
+    w = _tiny(K=2, sizes=(P,), h_lo=1e-3)
+    _say(f"problem data P={P}")
+    with A.Adpsgd.from_workload(w) as eng:
+        h = eng.h.double().cpu().numpy()
+        xs = eng.xstar.double().cpu().numpy()
+        assert not eng.x.any() and not eng.m.any()
+    h_o, xs_o = oracle.problem_data(w)
+    assert rel_err(h, h_o) < 2e-6
+    assert np.max(np.abs(xs - xs_o) / np.maximum(1.0, np.abs(xs_o))) < 2e-6
+
+
+# ---------------------------------------------------------------- local steps and sync
+
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16, 32])
+@pytest.mark.parametrize("sizes", [(4096 * 3 + 4,), (5000, 3, 5001, 993)])   # aligned / ragged P
+def test_local_steps_match_oracle(A, K, sizes):
+    w = _tiny(K=K, sizes=sizes)
+    n = 7
+    _say(f"local steps K={K} P={w.P}")
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.local_steps(n)
+        x = eng.x.double().cpu().numpy()
+        m = eng.m.double().cpu().numpy()
+        st = eng.get_state()
+    r = oracle.Oracle(w).run(n_steps=n)
+    assert r.n_syncs == 0 and st.t == n and st.cnt == n
+    assert max_rel_err(x, r.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(m, r.v, w.offsets()) < PARAM_TOL
+
+
+@pytest.mark.parametrize("K", [1, 3, 8, 32])
+@pytest.mark.parametrize("sizes", [(4096 * 3 + 4,), (5000, 3, 0, 5001, 993, 1), (8192, 4096, 12)])
+def test_average_matches_oracle(A, K, sizes):
+    w = _tiny(K=K, sizes=sizes)
+    n = 6
+    _say(f"average K={K} sizes={sizes}")
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.local_steps(n)
+        var = eng.average()
+        x = eng.x.double().cpu().numpy()
+        m = eng.m.double().cpu().numpy()
+        assert eng.get_state().cnt == 0
+    o = oracle.Oracle(w)
+    r = o.run(n_steps=n)
+    S_o, var_o = o.average(r.x)
+    off = w.offsets()
+    assert all(np.array_equal(x[k], x[0]) for k in range(K))   # every replica holds the mean
+    assert max_rel_err(x, r.x, off) < PARAM_TOL
+    assert max_rel_err(m, r.v, off) < PARAM_TOL                # momentum untouched
+    if K == 1:
+        assert np.all(var == 0.0)
+    empty = np.diff(off) == 0
+    assert np.all(var[empty] == 0.0)
+    assert rel_err(var[~empty], var_o[~empty]) < VAR_TOL
+
+
+@pytest.mark.parametrize("K", [2, 5, 8, 32])
+def test_fused_sync_equals_step_then_sync(A, K):
+    w = _tiny(K=K, sizes=(4099, 1, 8000, 6))
+    _say(f"fused vs separate K={K}")
+    with A.Adpsgd.from_workload(w) as a, A.Adpsgd.from_workload(w) as b:
+        a.local_steps(4); va = a.step_average()
+        b.local_steps(5); vb = b.average()
+        assert np.array_equal(va, vb)
+        assert a.get_state().t == b.get_state().t == 5
+        import torch
+        assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
+
+
+def test_second_sync_has_zero_variance(A):
+    w = _tiny(K=8, sizes=(3000, 5000))
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.local_steps(3)
+        v1 = eng.average()
+        v2 = eng.average()
+    assert np.all(v1 > 0) and np.all(v2 == 0.0)
+
+
+# ---------------------------------------------------------------- whole runs
+
+@pytest.mark.parametrize("key", list(W.parity_workloads()))
+def test_run_matches_oracle(A, key):
+    w = W.parity_workloads()[key]
+    _say(f"run {key}: K={w.K} P={w.P} T={w.T} N={w.total_steps}")
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    recs = g["recs"]
+    assert g["n_syncs"] == r.n_syncs
+    assert np.array_equal(recs["t"], r.sync_t), "sync steps differ"
+    assert np.array_equal(recs["p"], r.sync_p)
+    assert rel_err(recs["S"], r.S) < VAR_TOL
+    assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
+    off = w.offsets()
+    assert max_rel_err(g["x"], r.x, off) < PARAM_TOL
+    assert max_rel_err(g["m"], r.v, off) < PARAM_TOL
+    assert g["state"].t == w.total_steps and g["state"].p == r.state.p
+    if w.period_mode == W.PERIOD_ADAPTIVE:
+        assert rel_err([g["state"].C2], [r.state.C2]) < VAR_TOL
+
+
+def test_period_one_replicas_stay_identical(A):
+    w = _tiny(K=8, sizes=(6000, 2001), p_init=1, total_steps=12)
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, _, n = eng.run(12)
+        x = eng.x.double().cpu().numpy()
+    assert n == 12 and list(recs["t"]) == list(range(12))
+    assert all(np.array_equal(x[k], x[0]) for k in range(8))
+    xbar, _ = oracle.Oracle(w).mean_trajectory(12)
+    assert max_rel_err(x[0], xbar, w.offsets()) < PARAM_TOL
+
+
+def test_runs_are_bit_reproducible(A):
+    w = W.parity_workloads()["many_small"].replace(total_steps=600, k_s=150)
+    a, b = gpu_run(w), gpu_run(w)
+    assert np.array_equal(a["x"], b["x"]) and np.array_equal(a["m"], b["m"])
+    assert np.array_equal(a["var"], b["var"]) and np.array_equal(a["recs"], b["recs"])
+
+
+def test_checkpoint_resume_is_bit_exact(A):
+    import torch
+    w = W.parity_workloads()["resnet18_like"].replace(total_steps=700, k_s=150)
+    full = gpu_run(w)
+    with A.Adpsgd.from_workload(w) as eng:
+        r1, v1, n1 = eng.run(350)
+        st = eng.get_state()
+        x_saved, m_saved = eng.x.clone(), eng.m.clone()
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.x.copy_(x_saved); eng.m.copy_(m_saved)
+        torch.cuda.synchronize()
+        eng.set_state(st)
+        r2, v2, n2 = eng.run(350)
+        x = eng.x.double().cpu().numpy()
+        m = eng.m.double().cpu().numpy()
+    assert n1 + n2 == full["n_syncs"]
+    assert np.array_equal(np.concatenate([r1, r2]), full["recs"])
+    assert np.array_equal(x, full["x"]) and np.array_equal(m, full["m"])
+
+
+def test_timing_counts_every_launch(A):
+    w = W.parity_workloads()["vgg16_adaptive"].replace(total_steps=100, k_s=20)
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.set_timing(True)
+        recs, _, n = eng.run(100)
+        tm = eng.get_timing()
+    assert tm.fused_launches == n and tm.segsum_launches == n
+    assert tm.step_launches == 100 - n and tm.average_launches == 0
+    assert tm.step_ms > 0 and tm.fused_ms > 0
+
+
+# ---------------------------------------------------------------- edge cases and errors
+
+def test_empty_parameter_vector(A):
+    w = _tiny(K=4, sizes=(0, 0), p_init=3, total_steps=10)
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, var, n = eng.run(10)
+    assert n == 3 and np.all(var == 0.0) and np.all(recs["S"] == 0.0)
+
+
+def test_single_worker_has_zero_variance(A):
+    w = _tiny(K=1, sizes=(777, 4096), p_init=4, total_steps=30,
+              period_mode=W.PERIOD_ADAPTIVE, k_s=8)
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    assert np.all(g["var"] == 0.0)
+    assert np.array_equal(g["recs"]["t"], r.sync_t)
+    assert max_rel_err(g["x"], r.x, w.offsets()) < PARAM_TOL
+
+
+def test_divergence_reports_non_finite_variance(A):
+    w = _tiny(K=4, sizes=(4096,), lr0=50.0, p_init=40, total_steps=200,
+              period_mode=W.PERIOD_ADAPTIVE, k_s=0)
+    with A.Adpsgd.from_workload(w) as eng:
+        with pytest.raises(A.AdpsgdError) as e:
+            eng.run(200)
+        assert e.value.code == A.ENONFINITE
+        st = eng.get_state()
+        assert st.p == 40 and st.t >= 40
+
+
+def test_invalid_calls_leave_context_unchanged(A):
+    import torch
+    w = _tiny(K=2, sizes=(1024,))
+    with A.Adpsgd.from_workload(w) as eng:
+        with pytest.raises(A.AdpsgdError) as e:
+            eng.schedule(np.zeros(1))
+        assert e.value.code == A.ESTATE
+        for bad in (-1,):
+            with pytest.raises(A.AdpsgdError):
+                eng.local_steps(bad)
+        st = eng.get_state()
+        bad_state = A.adpsgd_state(t=-1, cnt=0, nC2=0, C2=0.0, p=1)
+        with pytest.raises(A.AdpsgdError):
+            eng.set_state(bad_state)
+        assert eng.get_state().t == st.t
+        # a misaligned replica pointer is refused before anything runs
+        buf = A.adpsgd_buffers(x=eng.x.data_ptr() + 4, m=eng.m.data_ptr(), h=eng.h.data_ptr(),
+                               xstar=eng.xstar.data_ptr(), workspace=eng.workspace.data_ptr(),
+                               workspace_bytes=eng.workspace.numel(),
+                               stream=torch.cuda.current_stream().cuda_stream)
+        with pytest.raises(A.AdpsgdError) as e:
+            A.adpsgd_init(2, 1024, [0, 1024], eng.hp, buf)
+        assert e.value.code == A.EINVAL
