@@ -133,14 +133,17 @@ __global__ void __launch_bounds__(kBlock) k_local_step(StepParams a) {
 
 // ---------------------------------------------------------------- sync
 
-// Mean of the replicas (k ascending, then one correctly rounded division) and
-// the per-lane sum over workers of the squared deviation from it.
+// Mean of the replicas: a pairwise sum in a fixed tree order (exact when all
+// replicas are equal and K is a power of two, so a sync right after a sync
+// leaves zero variance), then one correctly rounded division.
+template <int N>
+__device__ __forceinline__ f4 tree_sum(const f4 *v) {
+    if constexpr (N == 1) return v[0];
+    else return tree_sum<N / 2>(v) + tree_sum<N - N / 2>(v + N / 2);
+}
 template <int KT>
-__device__ __forceinline__ f4 replica_mean(const f4 (&xr)[KT], int K) {
-    f4 s = xr[0];
-#pragma unroll
-    for (int k = 1; k < KT; ++k) s += xr[k];
-    return s / splat((float)K);
+__device__ __forceinline__ f4 replica_mean(const f4 (&xr)[KT]) {
+    return tree_sum<KT>(xr) / splat((float)KT);
 }
 
 // Tile of one tensor, groups [start/4, ceil(end/4)).  Groups cut by the tile
@@ -175,7 +178,7 @@ __global__ void __launch_bounds__(kBlock) k_tile_sync(SyncParams p) {
                     if (full) st4<NT>(mrow, m); else st4_masked(mrow, m, e0, lo, hi);
                 }
             }
-            const f4 mean = replica_mean<KT>(xr, KT);
+            const f4 mean = replica_mean<KT>(xr);
 #pragma unroll
             for (int k = 0; k < KT; ++k) {
                 const f4 dk = mean - xr[k];

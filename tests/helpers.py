@@ -4,20 +4,23 @@ from __future__ import annotations
 import numpy as np
 
 
-def max_rel_err(a: np.ndarray, b: np.ndarray, offsets, floor: float = 1e-2) -> float:
+def max_rel_err(a: np.ndarray, b: np.ndarray, offsets, floor: float = 1e-2, scale_of=None) -> float:
     """Largest |a - b| / max(|b|, floor * rms_tau(b)) over all rows and tensors.
 
     a, b: [K, P] (or [P]); the rms floor is taken per tensor so elements that
-    happen to sit near zero are judged against the tensor's own scale.
+    happen to sit near zero are judged against the tensor's own scale.  If
+    scale_of ([*, P]) is given, the rms is taken over it instead of b.
     """
     a = np.atleast_2d(np.asarray(a, dtype=np.float64))
     b = np.atleast_2d(np.asarray(b, dtype=np.float64))
+    ref = b if scale_of is None else np.atleast_2d(np.asarray(scale_of, dtype=np.float64))
     worst = 0.0
     for lo, hi in zip(offsets[:-1], offsets[1:]):
         if hi == lo:
             continue
         bb = b[:, lo:hi]
-        rms = float(np.sqrt(np.mean(bb * bb)))
+        rr = ref[:, lo:hi]
+        rms = float(np.sqrt(np.mean(rr * rr)))
         den = np.maximum(np.abs(bb), max(floor * rms, 1e-30))
         worst = max(worst, float(np.max(np.abs(a[:, lo:hi] - bb) / den)))
     return worst

@@ -17,6 +17,10 @@ pytestmark = pytest.mark.gpu
 
 PARAM_TOL = 1e-4
 VAR_TOL = 1e-3
+# Momentum buffers are zero-mean, noise-driven state: an element's error is
+# set by the fp32 rounding of the x it integrates, not by its own size, so m is
+# judged against max(|m|, rms of its tensor) instead of a 1e-2 rms floor.
+MOM_FLOOR = 1.0
 
 
 def _say(msg):
@@ -99,7 +103,7 @@ def test_local_steps_match_oracle(A, K, sizes):
     r = oracle.Oracle(w).run(n_steps=n)
     assert r.n_syncs == 0 and st.t == n and st.cnt == n
     assert max_rel_err(x, r.x, w.offsets()) < PARAM_TOL
-    assert max_rel_err(m, r.v, w.offsets()) < PARAM_TOL
+    assert max_rel_err(m, r.v, w.offsets(), floor=MOM_FLOOR) < PARAM_TOL
 
 
 @pytest.mark.parametrize("K", [1, 3, 8, 32])
@@ -120,7 +124,7 @@ def test_average_matches_oracle(A, K, sizes):
     off = w.offsets()
     assert all(np.array_equal(x[k], x[0]) for k in range(K))   # every replica holds the mean
     assert max_rel_err(x, r.x, off) < PARAM_TOL
-    assert max_rel_err(m, r.v, off) < PARAM_TOL                # momentum untouched
+    assert max_rel_err(m, r.v, off, floor=MOM_FLOOR) < PARAM_TOL   # momentum untouched
     if K == 1:
         assert np.all(var == 0.0)
     empty = np.diff(off) == 0
@@ -141,13 +145,18 @@ def test_fused_sync_equals_step_then_sync(A, K):
         assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
 
 
-def test_second_sync_has_zero_variance(A):
-    w = _tiny(K=8, sizes=(3000, 5000))
+@pytest.mark.parametrize("K", [3, 8, 32])
+def test_second_sync_has_zero_variance(A, K):
+    w = _tiny(K=K, sizes=(3000, 5000))
     with A.Adpsgd.from_workload(w) as eng:
         eng.local_steps(3)
         v1 = eng.average()
         v2 = eng.average()
-    assert np.all(v1 > 0) and np.all(v2 == 0.0)
+    assert np.all(v1 > 0)
+    if K & (K - 1) == 0:
+        assert np.all(v2 == 0.0)      # the pairwise mean of equal values is exact
+    else:
+        assert np.all(v2 <= 1e-9 * v1)  # one rounding of the mean per element
 
 
 # ---------------------------------------------------------------- whole runs
@@ -165,8 +174,11 @@ def test_run_matches_oracle(A, key):
     assert rel_err(recs["S"], r.S) < VAR_TOL
     assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
     off = w.offsets()
-    assert max_rel_err(g["x"], r.x, off) < PARAM_TOL
-    assert max_rel_err(g["m"], r.v, off) < PARAM_TOL
+    ex, em = max_rel_err(g["x"], r.x, off), max_rel_err(g["m"], r.v, off, floor=MOM_FLOOR)
+    _say(f"  {key}: {r.n_syncs} syncs, err x {ex:.2e} m {em:.2e} "
+         f"var {rel_err(g['var'], r.var):.2e}, min |margin| {np.nanmin(np.abs(recs['margin'])) if w.period_mode else float('nan'):.2e}")
+    assert ex < PARAM_TOL
+    assert em < PARAM_TOL
     assert g["state"].t == w.total_steps and g["state"].p == r.state.p
     if w.period_mode == W.PERIOD_ADAPTIVE:
         assert rel_err([g["state"].C2], [r.state.C2]) < VAR_TOL
@@ -187,7 +199,7 @@ def test_runs_are_bit_reproducible(A):
     w = W.parity_workloads()["many_small"].replace(total_steps=600, k_s=150)
     a, b = gpu_run(w), gpu_run(w)
     assert np.array_equal(a["x"], b["x"]) and np.array_equal(a["m"], b["m"])
-    assert np.array_equal(a["var"], b["var"]) and np.array_equal(a["recs"], b["recs"])
+    assert np.array_equal(a["var"], b["var"]) and a["recs"].tobytes() == b["recs"].tobytes()
 
 
 def test_checkpoint_resume_is_bit_exact(A):
@@ -206,7 +218,7 @@ def test_checkpoint_resume_is_bit_exact(A):
         x = eng.x.double().cpu().numpy()
         m = eng.m.double().cpu().numpy()
     assert n1 + n2 == full["n_syncs"]
-    assert np.array_equal(np.concatenate([r1, r2]), full["recs"])
+    assert np.concatenate([r1, r2]).tobytes() == full["recs"].tobytes()
     assert np.array_equal(x, full["x"]) and np.array_equal(m, full["m"])
 
 
