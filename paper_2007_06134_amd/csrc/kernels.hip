@@ -1,19 +1,24 @@
 // gfx950 kernels of the ADPSGD hot path.
 //
-//   k_local_step   one local step of every worker (Algorithm 2, lines 5-7):
-//                  a streaming pass over x and m, with the per-worker noisy
-//                  quadratic gradient generated in registers.
-//   k_tile_sync    the synchronization (Algorithm 2, lines 10-12) per tile of
-//                  one tensor: replica mean, per-element squared deviations
+//   k_local_step   one local step of every worker (Algorithm 2, lines 5-7): a
+//                  streaming pass over x and m with the noisy quadratic
+//                  gradient generated in registers.
+//   k_sync_lds     the synchronization (Algorithm 2, lines 10-12) on one tile
+//                  of one tensor: replica mean, per-element squared deviations
 //                  (the parameter variance of Section II-B), broadcast of the
 //                  mean; optionally fused behind the period's last local step
-//                  so the sync costs no extra pass over HBM.
-//   k_segsum       fixed-order sum of the tile partials of each tensor.
+//                  so a sync costs no extra pass over HBM.
+//   k_sync_loop    the same for a worker count without a compiled variant.
+//   k_seg_chunks,  fixed-order sums of the tile partials: per chunk of tiles,
+//   k_seg_tensors  then per tensor.
 //
-// Work unit: a group of four consecutive elements (one dwordx4 per row and one
-// Philox call per worker).  Every kernel is HBM-bound streaming work: no
-// atomics, no data-dependent control flow, and a fixed reduction order, so
-// results are bit-reproducible for a given (K, P, offsets).
+// Work unit: a group of four consecutive elements of one worker's row, moved
+// with one dwordx4 load and store and fed by one Philox call.  On MI355X a
+// stream of one dwordx4 access per thread over a large grid sustains far more
+// HBM bandwidth than threads that each walk many rows, so every thread owns a
+// single (group, worker) pair.  The K threads of a group exchange replicas
+// through LDS at a sync.  No atomics and a fixed reduction order make results
+// bit-reproducible for a given (K, P, offsets).
 #include <cmath>
 
 #include "kernels.hpp"
@@ -27,6 +32,9 @@ __device__ __forceinline__ f4 fma4(f4 a, f4 b, f4 c) {
 }
 __device__ __forceinline__ f4 splat(float v) { return f4{v, v, v, v}; }
 
+// Replica rows are touched once per step and never reused before the next
+// step, so with a working set beyond the on-chip caches they are streamed with
+// non-temporal loads and stores.
 template <bool NT>
 __device__ __forceinline__ f4 ld4(const float *p) {
     if constexpr (NT) return __builtin_nontemporal_load(reinterpret_cast<const f4 *>(p));
@@ -38,24 +46,25 @@ __device__ __forceinline__ void st4(float *p, f4 v) {
     else *reinterpret_cast<f4 *>(p) = v;
 }
 
-// Masked scalar access to the lanes of group g that lie in [lo, hi).
+// Masked scalar access to the lanes of a group that lie in [lo, hi).
+__device__ __forceinline__ bool in(int64_t e, int64_t lo, int64_t hi) { return e >= lo && e < hi; }
 __device__ __forceinline__ f4 ld4_masked(const float *base, int64_t e0, int64_t lo, int64_t hi) {
     f4 v = splat(0.0f);
-    if (e0 + 0 >= lo && e0 + 0 < hi) v.x = base[0];
-    if (e0 + 1 >= lo && e0 + 1 < hi) v.y = base[1];
-    if (e0 + 2 >= lo && e0 + 2 < hi) v.z = base[2];
-    if (e0 + 3 >= lo && e0 + 3 < hi) v.w = base[3];
+    if (in(e0 + 0, lo, hi)) v.x = base[0];
+    if (in(e0 + 1, lo, hi)) v.y = base[1];
+    if (in(e0 + 2, lo, hi)) v.z = base[2];
+    if (in(e0 + 3, lo, hi)) v.w = base[3];
     return v;
 }
 __device__ __forceinline__ void st4_masked(float *base, f4 v, int64_t e0, int64_t lo, int64_t hi) {
-    if (e0 + 0 >= lo && e0 + 0 < hi) base[0] = v.x;
-    if (e0 + 1 >= lo && e0 + 1 < hi) base[1] = v.y;
-    if (e0 + 2 >= lo && e0 + 2 < hi) base[2] = v.z;
-    if (e0 + 3 >= lo && e0 + 3 < hi) base[3] = v.w;
+    if (in(e0 + 0, lo, hi)) base[0] = v.x;
+    if (in(e0 + 1, lo, hi)) base[1] = v.y;
+    if (in(e0 + 2, lo, hi)) base[2] = v.z;
+    if (in(e0 + 3, lo, hi)) base[3] = v.w;
 }
 __device__ __forceinline__ f4 mask4(f4 v, int64_t e0, int64_t lo, int64_t hi) {
-    return f4{(e0 + 0 >= lo && e0 + 0 < hi) ? v.x : 0.0f, (e0 + 1 >= lo && e0 + 1 < hi) ? v.y : 0.0f,
-              (e0 + 2 >= lo && e0 + 2 < hi) ? v.z : 0.0f, (e0 + 3 >= lo && e0 + 3 < hi) ? v.w : 0.0f};
+    return f4{in(e0 + 0, lo, hi) ? v.x : 0.0f, in(e0 + 1, lo, hi) ? v.y : 0.0f,
+              in(e0 + 2, lo, hi) ? v.z : 0.0f, in(e0 + 3, lo, hi) ? v.w : 0.0f};
 }
 
 // Gradient noise of worker k at step t for group g.
@@ -72,159 +81,209 @@ __device__ __forceinline__ void sgd_update(const StepParams &a, f4 &x, f4 &m, f4
     x = fma4(splat(-a.gamma), m, x);
 }
 
-// Wave64 butterfly, then the four waves in a fixed order.  Valid on thread 0.
+// Sum over the block in a fixed order: wave64 butterfly, then the waves in
+// order.  Valid on thread 0.
+template <int WAVES>
 __device__ __forceinline__ double block_sum(double v) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    __shared__ double wave_sum[kBlock / 64];
-    if ((threadIdx.x & 63) == 0) wave_sum[threadIdx.x >> 6] = v;
-    __syncthreads();
-    double total = 0.0;
-    if (threadIdx.x == 0) {
+    if constexpr (WAVES == 1) {
+        return v;
+    } else {
+        __shared__ double wave_sum[WAVES];
+        if ((threadIdx.x & 63) == 0) wave_sum[threadIdx.x >> 6] = v;
+        __syncthreads();
+        double total = 0.0;
+        if (threadIdx.x == 0) {
 #pragma unroll
-        for (int w = 0; w < kBlock / 64; ++w) total += wave_sum[w];
+            for (int w = 0; w < WAVES; ++w) total += wave_sum[w];
+        }
+        return total;
     }
-    return total;
 }
 
 // ---------------------------------------------------------------- local step
 
-// One thread per group, the worker loop inside: h and x* are loaded once and
-// reused by all K workers; each worker's row costs one dwordx4 load and store
-// of x and of m.  KT > 0 fixes K at compile time (fully unrolled).
-template <int KT, bool VEC, bool NT>
+// Thread = (group g, worker k).  Blocks are ordered so that the K blocks of a
+// 256-group chunk are dispatched to the same XCD one after another (workgroups
+// go round-robin over the 8 XCDs): h and x* of the chunk come from HBM once and
+// from that XCD's L2 for the other K-1 workers.
+template <bool VEC, bool NT>
 __global__ void __launch_bounds__(kBlock) k_local_step(StepParams a) {
-    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t b = blockIdx.x;
+    const int64_t s = b >> 3;                        // position within the XCD
+    const int k = (int)(s % a.K);
+    const int64_t chunk = (s / a.K) * 8 + (b & 7);
+    const int64_t g = chunk * kBlock + threadIdx.x;
     if (g >= a.n_groups) return;
-    const int K = KT > 0 ? KT : a.K;
     const int64_t e0 = 4 * g;
+    float *xr = a.x + (int64_t)k * a.P + e0;
+    float *mr = a.m + (int64_t)k * a.P + e0;
     if constexpr (VEC) {
-        const f4 h = ld4<false>(a.h + e0);
-        const f4 xs = ld4<false>(a.xs + e0);
-        auto one_worker = [&](int k) {
-            float *xr = a.x + (int64_t)k * a.P + e0;
-            float *mr = a.m + (int64_t)k * a.P + e0;
-            f4 x = ld4<NT>(xr), m = ld4<NT>(mr);
-            sgd_update(a, x, m, h, xs, step_noise(a, g, k));
-            st4<NT>(xr, x);
-            st4<NT>(mr, m);
-        };
-        if constexpr (KT > 0) {
-#pragma unroll
-            for (int k = 0; k < KT; ++k) one_worker(k);
-        } else {
-            for (int k = 0; k < K; ++k) one_worker(k);
-        }
+        f4 x = ld4<NT>(xr), m = ld4<NT>(mr);
+        const f4 h = ld4<false>(a.h + e0), xs = ld4<false>(a.xs + e0);
+        sgd_update(a, x, m, h, xs, step_noise(a, g, k));
+        st4<NT>(xr, x);
+        st4<NT>(mr, m);
     } else {
-        // P not a multiple of 4: rows are not 16-byte aligned, so every access
-        // is a scalar one, masked to [0, P) in the ragged last group
-        const f4 h = ld4_masked(a.h + e0, e0, 0, a.P);
-        const f4 xs = ld4_masked(a.xs + e0, e0, 0, a.P);
-        for (int k = 0; k < K; ++k) {
-            float *xr = a.x + (int64_t)k * a.P + e0;
-            float *mr = a.m + (int64_t)k * a.P + e0;
-            f4 x = ld4_masked(xr, e0, 0, a.P), m = ld4_masked(mr, e0, 0, a.P);
-            sgd_update(a, x, m, h, xs, step_noise(a, g, k));
-            st4_masked(xr, x, e0, 0, a.P);
-            st4_masked(mr, m, e0, 0, a.P);
-        }
+        // P not a multiple of 4: rows are not 16-byte aligned; scalar accesses,
+        // masked to [0, P) in the ragged last group
+        f4 x = ld4_masked(xr, e0, 0, a.P), m = ld4_masked(mr, e0, 0, a.P);
+        const f4 h = ld4_masked(a.h + e0, e0, 0, a.P), xs = ld4_masked(a.xs + e0, e0, 0, a.P);
+        sgd_update(a, x, m, h, xs, step_noise(a, g, k));
+        st4_masked(xr, x, e0, 0, a.P);
+        st4_masked(mr, m, e0, 0, a.P);
     }
 }
 
 // ---------------------------------------------------------------- sync
 
-// Mean of the replicas: a pairwise sum in a fixed tree order (exact when all
-// replicas are equal and K is a power of two, so a sync right after a sync
-// leaves zero variance), then one correctly rounded division.
+// Pairwise sum of rows[base .. base+N) at one lane, in a fixed tree order (left
+// half, right half).  Exact when all rows are equal and N is a power of two,
+// so a sync right after a sync leaves zero variance.  Depth-first evaluation
+// keeps only O(log N) partial sums live.
 template <int N>
-__device__ __forceinline__ f4 tree_sum(const f4 *v) {
-    if constexpr (N == 1) return v[0];
-    else return tree_sum<N / 2>(v) + tree_sum<N - N / 2>(v + N / 2);
-}
-template <int KT>
-__device__ __forceinline__ f4 replica_mean(const f4 (&xr)[KT]) {
-    return tree_sum<KT>(xr) / splat((float)KT);
+__device__ __forceinline__ f4 tree_sum_lds(const f4 (*rows)[64], int lane, int base) {
+    if constexpr (N == 1) {
+        return rows[base][lane];
+    } else {
+        const f4 l = tree_sum_lds<N / 2>(rows, lane, base);
+        const f4 r = tree_sum_lds<N - N / 2>(rows, lane, base + N / 2);
+        return l + r;
+    }
 }
 
-// Tile of one tensor, groups [start/4, ceil(end/4)).  Groups cut by the tile
-// bounds (tensor boundaries that are not multiples of 4, or an unaligned P)
-// go through masked scalar accesses; the arithmetic per element is the same.
+// One tile (at most 64 groups, one per lane) of one tensor.  Wave w owns the
+// rows k = w, w + W, ... (W = min(K, 16) waves, R = K / W rows each).  Each
+// thread steps its rows (if fused), publishes them in LDS, reads all K rows of
+// its lane back to form the mean in a fixed order (the same bits in every
+// thread), then writes the mean over its rows and sums its squared deviations.
+// Lanes of groups cut by the tile bounds use masked scalar accesses.
 template <int KT, bool VEC, bool NT, bool FUSED>
-__global__ void __launch_bounds__(kBlock) k_tile_sync(SyncParams p) {
+__global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParams p) {
+    constexpr int W = KT < 16 ? KT : 16;
+    constexpr int R = KT / W;
+    __shared__ f4 rows[KT][64];
+    const StepParams &a = p.s;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const Tile tile = p.tiles[blockIdx.x];
+    const int64_t lo = tile.start, hi = tile.start + tile.len;
+    const int64_t g = (lo >> 2) + lane;
+    const int64_t e0 = 4 * g;
+    const bool active = e0 < hi;
+    const bool full = VEC && e0 >= lo && e0 + 4 <= hi;
+    f4 xr[R];
+    if (active) {
+        f4 h = splat(0.0f), xs = splat(0.0f);
+        f4 m[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
+            xr[r] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
+            if (FUSED) {
+                float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
+                m[r] = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
+            }
+        }
+        if (FUSED) {
+            if (full) { h = ld4<false>(a.h + e0); xs = ld4<false>(a.xs + e0); }
+            else { h = ld4_masked(a.h + e0, e0, lo, hi); xs = ld4_masked(a.xs + e0, e0, lo, hi); }
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int k = w + W * r;
+                sgd_update(a, xr[r], m[r], h, xs, step_noise(a, g, k));
+                float *mrow = a.m + (int64_t)k * a.P + e0;
+                if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) rows[w + W * r][lane] = xr[r];
+    }
+    __syncthreads();
+    double acc = 0.0;
+    if (active) {
+        const f4 mean = tree_sum_lds<KT>(rows, lane, 0) / splat((float)KT);
+        f4 dev2 = splat(0.0f);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const f4 dk = mean - xr[r];
+            dev2 = fma4(dk, dk, dev2);
+            float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
+            if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
+        }
+        if (!full) dev2 = mask4(dev2, e0, lo, hi);
+        acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
+    }
+    const double total = block_sum<W>(acc);
+    if (threadIdx.x == 0) p.partials[blockIdx.x] = total;
+}
+
+// Any K: one wave per tile, lane = group, the workers walked in a loop.  The
+// first pass sums the replicas (stepping and storing them if fused), the
+// second re-reads them for the deviations and writes the mean.
+template <bool VEC, bool FUSED>
+__global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     const StepParams &a = p.s;
     const Tile tile = p.tiles[blockIdx.x];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
-    const int64_t g_end = (hi + 3) >> 2;
+    const int64_t g = (lo >> 2) + threadIdx.x;
+    const int64_t e0 = 4 * g;
     double acc = 0.0;
-    for (int64_t g = (lo >> 2) + threadIdx.x; g < g_end; g += kBlock) {
-        const int64_t e0 = 4 * g;
+    if (e0 < hi) {
         const bool full = VEC && e0 >= lo && e0 + 4 <= hi;
         f4 h = splat(0.0f), xs = splat(0.0f);
         if (FUSED) {
             if (full) { h = ld4<false>(a.h + e0); xs = ld4<false>(a.xs + e0); }
             else { h = ld4_masked(a.h + e0, e0, lo, hi); xs = ld4_masked(a.xs + e0, e0, lo, hi); }
         }
+        f4 s = splat(0.0f);
+        for (int k = 0; k < a.K; ++k) {
+            float *xrow = a.x + (int64_t)k * a.P + e0;
+            f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
+            if (FUSED) {
+                float *mrow = a.m + (int64_t)k * a.P + e0;
+                f4 m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
+                sgd_update(a, x, m, h, xs, step_noise(a, g, k));
+                if (full) { st4<false>(mrow, m); st4<false>(xrow, x); }
+                else { st4_masked(mrow, m, e0, lo, hi); st4_masked(xrow, x, e0, lo, hi); }
+            }
+            s = (k == 0) ? x : s + x;
+        }
+        const f4 mean = s / splat((float)a.K);
         f4 dev2 = splat(0.0f);
-        if constexpr (KT > 0) {
-            f4 xr[KT];
-#pragma unroll
-            for (int k = 0; k < KT; ++k) {
-                float *xrow = a.x + (int64_t)k * a.P + e0;
-                xr[k] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
-                if (FUSED) {
-                    float *mrow = a.m + (int64_t)k * a.P + e0;
-                    f4 m = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
-                    sgd_update(a, xr[k], m, h, xs, step_noise(a, g, k));
-                    if (full) st4<NT>(mrow, m); else st4_masked(mrow, m, e0, lo, hi);
-                }
-            }
-            const f4 mean = replica_mean<KT>(xr);
-#pragma unroll
-            for (int k = 0; k < KT; ++k) {
-                const f4 dk = mean - xr[k];
-                dev2 = fma4(dk, dk, dev2);
-                float *xrow = a.x + (int64_t)k * a.P + e0;
-                if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
-            }
-        } else {
-            // K not fixed at compile time: sum in a first pass (stepping and
-            // storing the new replicas if fused), re-read them in a second.
-            f4 s = splat(0.0f);
-            for (int k = 0; k < a.K; ++k) {
-                float *xrow = a.x + (int64_t)k * a.P + e0;
-                f4 x = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
-                if (FUSED) {
-                    float *mrow = a.m + (int64_t)k * a.P + e0;
-                    f4 m = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
-                    sgd_update(a, x, m, h, xs, step_noise(a, g, k));
-                    if (full) { st4<NT>(mrow, m); st4<NT>(xrow, x); }
-                    else { st4_masked(mrow, m, e0, lo, hi); st4_masked(xrow, x, e0, lo, hi); }
-                }
-                s = (k == 0) ? x : s + x;
-            }
-            const f4 mean = s / splat((float)a.K);
-            for (int k = 0; k < a.K; ++k) {
-                float *xrow = a.x + (int64_t)k * a.P + e0;
-                const f4 x = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
-                const f4 dk = mean - x;
-                dev2 = fma4(dk, dk, dev2);
-                if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
-            }
+        for (int k = 0; k < a.K; ++k) {
+            float *xrow = a.x + (int64_t)k * a.P + e0;
+            const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
+            const f4 dk = mean - x;
+            dev2 = fma4(dk, dk, dev2);
+            if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
         }
         if (!full) dev2 = mask4(dev2, e0, lo, hi);
-        acc += ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
+        acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
     }
-    const double total = block_sum(acc);
+    const double total = block_sum<1>(acc);
     if (threadIdx.x == 0) p.partials[blockIdx.x] = total;
 }
 
-__global__ void __launch_bounds__(kBlock) k_segsum(const int32_t *tile_begin, const double *partials,
-                                                   double *var, int32_t K) {
-    const int32_t tau = blockIdx.x;
-    const int32_t b = tile_begin[tau], e = tile_begin[tau + 1];
+// Level 1: the tiles of chunk c are [chunks[c].first, + count), all in one tensor.
+__global__ void __launch_bounds__(kBlock) k_seg_chunks(const Chunk *chunks, const double *tile_partials,
+                                                      double *chunk_partials) {
+    const Chunk c = chunks[blockIdx.x];
     double acc = 0.0;
-    for (int32_t i = b + (int32_t)threadIdx.x; i < e; i += kBlock) acc += partials[i];
-    const double total = block_sum(acc);
+    for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) acc += tile_partials[c.first + i];
+    const double total = block_sum<kBlock / 64>(acc);
+    if (threadIdx.x == 0) chunk_partials[blockIdx.x] = total;
+}
+
+// Level 2: var[tau] = (sum of the partials of tau's chunks) / K; tau's chunks
+// are [chunk_begin[tau], chunk_begin[tau+1]).
+__global__ void __launch_bounds__(kBlock) k_seg_tensors(const int32_t *chunk_begin, const double *chunk_partials,
+                                                       double *var, int32_t K) {
+    const int32_t tau = blockIdx.x;
+    const int32_t b = chunk_begin[tau], e = chunk_begin[tau + 1];
+    double acc = 0.0;
+    for (int32_t i = b + (int32_t)threadIdx.x; i < e; i += kBlock) acc += chunk_partials[i];
+    const double total = block_sum<kBlock / 64>(acc);
     if (threadIdx.x == 0) var[tau] = total / (double)K;
 }
 
@@ -262,47 +321,38 @@ __global__ void __launch_bounds__(kBlock) k_normal_dump(RoundKeys rk, uint32_t c
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
 
 template <int KT>
-hipError_t step_dispatch(const StepParams &p, bool vec, bool nt, hipStream_t st) {
-    const dim3 grid(blocks_for(p.n_groups)), block(kBlock);
-    if (vec && nt) k_local_step<KT, true, true><<<grid, block, 0, st>>>(p);
-    else if (vec) k_local_step<KT, true, false><<<grid, block, 0, st>>>(p);
-    else k_local_step<KT, false, false><<<grid, block, 0, st>>>(p);
-    return hipGetLastError();
-}
-
-template <int KT>
-hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt,
-                         hipStream_t st) {
-    const dim3 grid((unsigned)n_tiles), block(kBlock);
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt, hipStream_t st) {
+    constexpr int threads = 64 * (KT < 16 ? KT : 16);
+    const dim3 grid((unsigned)n_tiles), block(threads);
     if (fused) {
-        if (vec && nt) k_tile_sync<KT, true, true, true><<<grid, block, 0, st>>>(p);
-        else if (vec) k_tile_sync<KT, true, false, true><<<grid, block, 0, st>>>(p);
-        else k_tile_sync<KT, false, false, true><<<grid, block, 0, st>>>(p);
+        if (vec && nt) k_sync_lds<KT, true, true, true><<<grid, block, 0, st>>>(p);
+        else if (vec) k_sync_lds<KT, true, false, true><<<grid, block, 0, st>>>(p);
+        else k_sync_lds<KT, false, false, true><<<grid, block, 0, st>>>(p);
     } else {
-        if (vec && nt) k_tile_sync<KT, true, true, false><<<grid, block, 0, st>>>(p);
-        else if (vec) k_tile_sync<KT, true, false, false><<<grid, block, 0, st>>>(p);
-        else k_tile_sync<KT, false, false, false><<<grid, block, 0, st>>>(p);
+        if (vec && nt) k_sync_lds<KT, true, true, false><<<grid, block, 0, st>>>(p);
+        else if (vec) k_sync_lds<KT, true, false, false><<<grid, block, 0, st>>>(p);
+        else k_sync_lds<KT, false, false, false><<<grid, block, 0, st>>>(p);
     }
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t st) {
-    if (p.n_groups <= 0) return hipSuccess;
-    switch (p.K) {
-    case 1: return step_dispatch<1>(p, vec, nt, st);
-    case 2: return step_dispatch<2>(p, vec, nt, st);
-    case 4: return step_dispatch<4>(p, vec, nt, st);
-    case 8: return step_dispatch<8>(p, vec, nt, st);
-    case 16: return step_dispatch<16>(p, vec, nt, st);
-    case 32: return step_dispatch<32>(p, vec, nt, st);
-    default: return step_dispatch<0>(p, vec, nt, st);
-    }
+int64_t local_step_blocks(int64_t n_groups, int32_t K) {
+    const int64_t chunks = (n_groups + kBlock - 1) / kBlock;
+    return ((chunks + 7) / 8) * 8 * (int64_t)K;
 }
 
-hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt,
-                            hipStream_t st) {
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t st) {
+    if (p.n_groups <= 0) return hipSuccess;
+    const dim3 grid((unsigned)local_step_blocks(p.n_groups, p.K)), block(kBlock);
+    if (vec && nt) k_local_step<true, true><<<grid, block, 0, st>>>(p);
+    else if (vec) k_local_step<true, false><<<grid, block, 0, st>>>(p);
+    else k_local_step<false, false><<<grid, block, 0, st>>>(p);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt, hipStream_t st) {
     if (n_tiles <= 0) return hipSuccess;
     switch (p.s.K) {
     case 1: return sync_dispatch<1>(p, n_tiles, fused, vec, nt, st);
@@ -311,14 +361,30 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bo
     case 8: return sync_dispatch<8>(p, n_tiles, fused, vec, nt, st);
     case 16: return sync_dispatch<16>(p, n_tiles, fused, vec, nt, st);
     case 32: return sync_dispatch<32>(p, n_tiles, fused, vec, nt, st);
-    default: return sync_dispatch<0>(p, n_tiles, fused, vec, nt, st);
+    default: {
+        const dim3 grid((unsigned)n_tiles), block(64);
+        if (fused) {
+            if (vec) k_sync_loop<true, true><<<grid, block, 0, st>>>(p);
+            else k_sync_loop<false, true><<<grid, block, 0, st>>>(p);
+        } else {
+            if (vec) k_sync_loop<true, false><<<grid, block, 0, st>>>(p);
+            else k_sync_loop<false, false><<<grid, block, 0, st>>>(p);
+        }
+        return hipGetLastError();
+    }
     }
 }
 
-hipError_t launch_segsum(const int32_t *tile_begin, const double *partials, double *var, int32_t T,
-                         int32_t K, hipStream_t st) {
+hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
+                         const double *tile_partials, double *chunk_partials, double *var, int32_t T, int32_t K,
+                         hipStream_t st) {
+    if (n_chunks > 0) {
+        k_seg_chunks<<<dim3((unsigned)n_chunks), dim3(kBlock), 0, st>>>(chunks, tile_partials, chunk_partials);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (T <= 0) return hipSuccess;
-    k_segsum<<<dim3((unsigned)T), dim3(kBlock), 0, st>>>(tile_begin, partials, var, K);
+    k_seg_tensors<<<dim3((unsigned)T), dim3(kBlock), 0, st>>>(chunk_begin, chunk_partials, var, K);
     return hipGetLastError();
 }
 

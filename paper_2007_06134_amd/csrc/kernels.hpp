@@ -7,14 +7,22 @@
 
 namespace adpsgd {
 
-constexpr int kBlock = 256;          // threads per workgroup: four wave64s
-constexpr int64_t kTileElems = 4096; // max elements per sync tile (multiple of 4)
+constexpr int kBlock = 256;          // threads per workgroup of the streaming kernels
+constexpr int64_t kTileElems = 256;  // sync tiles are cut at multiples of 256 elements,
+                                     // so a tile spans at most 64 float4 groups (one wave)
+constexpr int32_t kChunkTiles = 1024;  // tiles per first-level chunk of the variance sum
 
 // One sync tile: a contiguous element range inside one tensor.
 struct Tile {
     int64_t start;
     int32_t len;
     int32_t tensor;
+};
+
+// Consecutive tiles of one tensor whose partials are summed together.
+struct Chunk {
+    int32_t first;
+    int32_t count;
 };
 
 // Everything a local step needs.  Replicas are rows of x/m with stride P.
@@ -37,15 +45,19 @@ struct SyncParams {
     double *partials;  // [n_tiles] sum over the tile of sum_k (xbar - x_k)^2
 };
 
+// Grid size of the local step for n_groups groups and K workers.
+int64_t local_step_blocks(int64_t n_groups, int32_t K);
 // vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4.
 hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, hipStream_t st);
 // fused = true: the local step and the sync in one pass.
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool vec,
                             bool nontemporal, hipStream_t st);
-// var[tau] = (sum of partials of tau's tiles) / K, tiles of tau are
-// [tile_begin[tau], tile_begin[tau+1]).
-hipError_t launch_segsum(const int32_t *tile_begin, const double *partials, double *var,
-                         int32_t T, int32_t K, hipStream_t st);
+// chunk_partials[c] = sum of the tile partials of chunk c; then
+// var[tau] = (sum of the partials of tau's chunks) / K, where tau's chunks are
+// [chunk_begin[tau], chunk_begin[tau+1]).
+hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
+                         const double *tile_partials, double *chunk_partials, double *var, int32_t T,
+                         int32_t K, hipStream_t st);
 hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, double h_lo,
                                double h_hi, hipStream_t st);
 hipError_t launch_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0,

@@ -54,40 +54,58 @@ bool shape_valid(int32_t K, int64_t P, int32_t T, const int64_t *off, std::strin
     return true;
 }
 
-// Tiles: each tensor [a, b) is cut at multiples of kTileElems, so interior
-// tile boundaries are float4-aligned and no tile crosses a tensor boundary.
-void build_tiles(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::vector<int32_t> *begin) {
-    tiles->clear();
-    begin->assign(T + 1, 0);
+// Tiles: each tensor [a, b) is cut at multiples of kTileElems, so no tile
+// crosses a tensor boundary and a tile spans at most kTileElems / 4 groups.
+// Chunks: runs of at most kChunkTiles consecutive tiles of one tensor.
+int64_t tiles_of(int64_t a, int64_t b) { return b > a ? (b + kTileElems - 1) / kTileElems - a / kTileElems : 0; }
+
+struct Plan {
+    int64_t n_tiles = 0, n_chunks = 0;
+};
+
+Plan count_plan(int32_t T, const int64_t *off) {
+    Plan pl;
     for (int32_t tau = 0; tau < T; ++tau) {
-        (*begin)[tau] = (int32_t)tiles->size();
+        const int64_t nt = tiles_of(off[tau], off[tau + 1]);
+        pl.n_tiles += nt;
+        pl.n_chunks += (nt + kChunkTiles - 1) / kChunkTiles;
+    }
+    return pl;
+}
+
+void build_plan(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::vector<Chunk> *chunks,
+                std::vector<int32_t> *chunk_begin) {
+    tiles->clear();
+    chunks->clear();
+    chunk_begin->assign(T + 1, 0);
+    for (int32_t tau = 0; tau < T; ++tau) {
+        (*chunk_begin)[tau] = (int32_t)chunks->size();
+        const int32_t first_tile = (int32_t)tiles->size();
         for (int64_t s = off[tau]; s < off[tau + 1];) {
             const int64_t e = std::min(off[tau + 1], (s / kTileElems + 1) * kTileElems);
             tiles->push_back(Tile{s, (int32_t)(e - s), tau});
             s = e;
         }
+        const int32_t n = (int32_t)tiles->size() - first_tile;
+        for (int32_t c = 0; c < n; c += kChunkTiles)
+            chunks->push_back(Chunk{first_tile + c, std::min(kChunkTiles, n - c)});
     }
-    (*begin)[T] = (int32_t)tiles->size();
-}
-
-int64_t count_tiles(int32_t T, const int64_t *off) {
-    int64_t n = 0;
-    for (int32_t tau = 0; tau < T; ++tau)
-        for (int64_t s = off[tau]; s < off[tau + 1]; s = std::min(off[tau + 1], (s / kTileElems + 1) * kTileElems))
-            ++n;
-    return n;
+    (*chunk_begin)[T] = (int32_t)chunks->size();
 }
 
 struct Layout {
-    size_t tiles, tile_begin, partials, var, total;
+    size_t tiles, chunks, chunk_begin, tile_partials, chunk_partials, var, total;
 };
 
-Layout layout_for(int64_t n_tiles, int32_t T) {
+Layout layout_for(const Plan &pl, int32_t T) {
+    auto at_least_one = [](int64_t n) { return (size_t)std::max<int64_t>(n, 1); };
     Layout l;
     l.tiles = 0;
-    l.tile_begin = align_up(l.tiles + sizeof(Tile) * (size_t)std::max<int64_t>(n_tiles, 1), 256);
-    l.partials = align_up(l.tile_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
-    l.var = align_up(l.partials + sizeof(double) * (size_t)std::max<int64_t>(n_tiles, 1), 256);
+    l.chunks = align_up(l.tiles + sizeof(Tile) * at_least_one(pl.n_tiles), 256);
+    l.chunk_begin = align_up(l.chunks + sizeof(Chunk) * at_least_one(pl.n_chunks), 256);
+    l.tile_partials = align_up(l.chunk_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
+    l.chunk_partials = align_up(l.tile_partials + sizeof(double) * at_least_one(pl.n_tiles), 256);
+    l.var = align_up(l.chunk_partials + sizeof(double) * at_least_one(pl.n_chunks), 256);
     l.total = align_up(l.var + sizeof(double) * (size_t)kRing * (size_t)T, 256);
     return l;
 }
@@ -120,20 +138,23 @@ struct adpsgd_ctx {
     int32_t T = 0;
     std::vector<int64_t> offsets;
     std::vector<Tile> tiles;
-    std::vector<int32_t> tile_begin;
+    std::vector<Chunk> chunks;
+    std::vector<int32_t> chunk_begin;
     adpsgd_hparams hp{};
     adpsgd_buffers buf{};
     hipStream_t stream = nullptr;
     int device = 0;
     Tile *d_tiles = nullptr;
-    int32_t *d_tile_begin = nullptr;
-    double *d_partials = nullptr;
+    Chunk *d_chunks = nullptr;
+    int32_t *d_chunk_begin = nullptr;
+    double *d_tile_partials = nullptr;
+    double *d_chunk_partials = nullptr;
     double *d_var = nullptr;        // [kRing][T] device
     double *h_var = nullptr;        // [kRing][T] pinned host
     hipEvent_t ring_ev[kRing] = {};
     adpsgd_state st{};
     bool vec = true;                // P % 4 == 0: dwordx4 rows
-    bool nontemporal = false;
+    bool nontemporal = false;       // stream x and m past the caches (large working sets)
     RoundKeys rk{};
     bool timing = false;
     std::deque<TimedLaunch> timed;
@@ -247,7 +268,7 @@ int enqueue_sync(adpsgd_ctx *c, bool fused, int64_t t, int slot) {
     SyncParams sp;
     sp.s = step_params(c, t);
     sp.tiles = c->d_tiles;
-    sp.partials = c->d_partials;
+    sp.partials = c->d_tile_partials;
     const int64_t n_tiles = (int64_t)c->tiles.size();
     int rc = timed_launch(c, fused ? kFused : kAverage, [&] {
         return launch_tile_sync(sp, n_tiles, fused, c->vec, c->nontemporal, c->stream);
@@ -255,7 +276,8 @@ int enqueue_sync(adpsgd_ctx *c, bool fused, int64_t t, int slot) {
     if (rc) return rc;
     double *dv = c->d_var + (size_t)slot * c->T;
     rc = timed_launch(c, kSegsum, [&] {
-        return launch_segsum(c->d_tile_begin, c->d_partials, dv, c->T, c->K, c->stream);
+        return launch_segsum(c->d_chunks, (int64_t)c->chunks.size(), c->d_chunk_begin, c->d_tile_partials,
+                             c->d_chunk_partials, dv, c->T, c->K, c->stream);
     });
     if (rc) return rc;
     HIP_TRY(hipMemcpyAsync(c->h_var + (size_t)slot * c->T, dv, sizeof(double) * c->T, hipMemcpyDeviceToHost,
@@ -282,7 +304,7 @@ extern "C" const char *adpsgd_last_error(void) { return g_last_error.c_str(); }
 extern "C" size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const int64_t *offsets) {
     std::string why;
     if (!shape_valid(K, P, T, offsets, &why)) return 0;
-    return layout_for(count_tiles(T, offsets), T).total;
+    return layout_for(count_plan(T, offsets), T).total;
 }
 
 extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t T, const adpsgd_hparams *hp,
@@ -297,9 +319,10 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be non-NULL");
     if (!aligned(buf->x, 16) || !aligned(buf->m, 16) || !aligned(buf->h, 16) || !aligned(buf->xstar, 16))
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be 16-byte aligned");
-    const int64_t n_tiles = count_tiles(T, offsets);
-    if (n_tiles >= (int64_t(1) << 31)) return fail(ADPSGD_EINVAL, "too many tiles");
-    const Layout lay = layout_for(n_tiles, T);
+    const Plan plan = count_plan(T, offsets);
+    if (plan.n_tiles >= (int64_t(1) << 31) || local_step_blocks((P + 3) / 4, K) >= (int64_t(1) << 31))
+        return fail(ADPSGD_EINVAL, "K * P too large for one launch");
+    const Layout lay = layout_for(plan, T);
     if (!buf->workspace || !aligned(buf->workspace, 256)) return fail(ADPSGD_EINVAL, "workspace must be 256-byte aligned");
     if (buf->workspace_bytes < lay.total)
         return fail(ADPSGD_EINVAL, "workspace too small: need " + std::to_string(lay.total) + " bytes");
@@ -310,16 +333,20 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->P = P;
     c->T = T;
     c->offsets.assign(offsets, offsets + T + 1);
-    build_tiles(T, offsets, &c->tiles, &c->tile_begin);
+    build_plan(T, offsets, &c->tiles, &c->chunks, &c->chunk_begin);
     c->hp = *hp;
     c->buf = *buf;
     c->stream = (hipStream_t)buf->stream;
     c->vec = (P % 4) == 0;
+    // x and m beyond the 256 MB last-level cache: stream them past the caches
+    c->nontemporal = (double)K * (double)P * 8.0 > 256.0 * 1024 * 1024;
     c->rk = round_keys(hp->seed);
     char *ws = (char *)buf->workspace;
     c->d_tiles = (Tile *)(ws + lay.tiles);
-    c->d_tile_begin = (int32_t *)(ws + lay.tile_begin);
-    c->d_partials = (double *)(ws + lay.partials);
+    c->d_chunks = (Chunk *)(ws + lay.chunks);
+    c->d_chunk_begin = (int32_t *)(ws + lay.chunk_begin);
+    c->d_tile_partials = (double *)(ws + lay.tile_partials);
+    c->d_chunk_partials = (double *)(ws + lay.chunk_partials);
     c->d_var = (double *)(ws + lay.var);
 
     auto bail = [&](hipError_t e, const char *what) {
@@ -339,9 +366,13 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         (e = hipMemcpyAsync(c->d_tiles, c->tiles.data(), sizeof(Tile) * c->tiles.size(), hipMemcpyHostToDevice,
                             c->stream)) != hipSuccess)
         return bail(e, "copy tile table");
-    if ((e = hipMemcpyAsync(c->d_tile_begin, c->tile_begin.data(), sizeof(int32_t) * (T + 1), hipMemcpyHostToDevice,
+    if (!c->chunks.empty() &&
+        (e = hipMemcpyAsync(c->d_chunks, c->chunks.data(), sizeof(Chunk) * c->chunks.size(), hipMemcpyHostToDevice,
                             c->stream)) != hipSuccess)
-        return bail(e, "copy tile offsets");
+        return bail(e, "copy chunk table");
+    if ((e = hipMemcpyAsync(c->d_chunk_begin, c->chunk_begin.data(), sizeof(int32_t) * (T + 1),
+                            hipMemcpyHostToDevice, c->stream)) != hipSuccess)
+        return bail(e, "copy chunk offsets");
     if ((e = hipMemsetAsync(c->d_var, 0, sizeof(double) * kRing * (size_t)T, c->stream)) != hipSuccess)
         return bail(e, "clear variance ring");
     if (P > 0) {
