@@ -53,15 +53,18 @@ __device__ __forceinline__ u4 philox10(u4 c, const RoundKeys &rk) {
 // Two Box-Muller normals from two words: radius sqrt(-2 ln u1) with
 // u1 = (hi24(a) + 1) 2^-24 in (0, 1] (never 0, so the log is finite) and angle
 // 2 pi u2 with u2 = hi24(b) 2^-24.  Both uniforms are exact in fp32.
-// sincospif takes the angle in half-turns, so 2 u2 is passed exactly.
+// The gfx950 transcendental instructions fit this form directly: v_log_f32 is
+// log2 (u1 >= 2^-24, so no denormal inputs), and v_sin_f32 / v_cos_f32 take
+// the angle in turns, so sin(2 pi u2) needs no range reduction.  This skips
+// the special-case handling of the libm-style wrappers, which this input range
+// never needs.
 __device__ __forceinline__ void box_muller2(uint32_t a, uint32_t b, float &z0, float &z1) {
     const float u1 = (float)((a >> 8) + 1u) * 0x1p-24f;
     const float u2 = (float)(b >> 8) * 0x1p-24f;
-    const float radius = sqrtf(-2.0f * logf(u1));
-    float s, c;
-    sincospif(2.0f * u2, &s, &c);
-    z0 = radius * c;
-    z1 = radius * s;
+    constexpr float kMinus2Ln2 = -1.38629436111989061883f;   // -2 ln 2
+    const float radius = __builtin_amdgcn_sqrtf(kMinus2Ln2 * __builtin_amdgcn_logf(u1));
+    z0 = radius * __builtin_amdgcn_cosf(u2);
+    z1 = radius * __builtin_amdgcn_sinf(u2);
 }
 
 __device__ __forceinline__ f4 normals4(u4 r) {
