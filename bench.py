@@ -53,7 +53,7 @@ def measured_traffic():
     return float(m_b.group(1))
 
 
-def cpu_baseline(w, P_sample=4_000_000, steps=40):
+def cpu_baseline(w, P_sample=8_000_000, steps=40):
     """The oracle, as it stands, on the first P_sample parameters of the same workload."""
     import oracle
     import workloads as W
