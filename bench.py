@@ -29,7 +29,6 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "local_step_k8_p138m_traffic.md")
-KERNEL_SRC = os.path.join(ROOT, "paper_2007_06134_amd", "csrc", "kernels.hip")
 
 
 def kernel_source_digest() -> str:
@@ -53,10 +52,9 @@ def measured_traffic():
     return float(m_b.group(1))
 
 
-def cpu_baseline(w, P_sample=8_000_000, steps=40):
+def cpu_baseline(w, P_sample=16_000_000, steps=80):
     """The oracle, as it stands, on the first P_sample parameters of the same workload."""
     import oracle
-    import workloads as W
     # keep whole tensors that fit, then cut the one that crosses P_sample
     sizes, acc = [], 0
     for s in w.sizes:

@@ -55,10 +55,16 @@ extern "C" {
 #define ADPSGD_LR_STEP 1   /* lr0 * 0.1 from t = floor(N/2), * 0.01 from floor(3N/4);
                               the paper's 10x decays at 1/2 and 3/4 of training (Sec. IV-B) */
 #define ADPSGD_LR_COSINE 2 /* lr0 * (1 + cos(pi t / N)) / 2                              */
+#define ADPSGD_LR_WARMUP_STEP 3 /* gradual warm-up then step decay (Sec. IV-C): with
+                              E = floor(N / 90) steps per "epoch", lr0 * (1 + floor(t / E))
+                              for t < 8 E (0.1 -> 0.8 for lr0 = 0.1), then 8 lr0, x0.1 from
+                              t = 30 E, x0.01 from t = 60 E                               */
 
 /* ---- period modes ----------------------------------------------------------- */
 #define ADPSGD_PERIOD_CONST 0    /* CPSGD, Algorithm 1: p = p_init throughout            */
 #define ADPSGD_PERIOD_ADAPTIVE 1 /* ADPSGD, Algorithm 2: C2 sampling, then p +- 1        */
+#define ADPSGD_PERIOD_ALG1 2     /* CPSGD with Algorithm 1's test: sync after every step t
+                                    with t mod p == 0 (after steps 0, p, 2p, ...)           */
 
 typedef struct adpsgd_ctx adpsgd_ctx; /* opaque, owned by the library */
 
@@ -82,6 +88,15 @@ typedef struct {
     int64_t k_s;         /* syncs after steps t < k_s sample C2 (Alg. 2, l. 13)   */
     double thr_lo;       /* p += 1 if S < thr_lo * gamma_t * C2 (paper: 0.7)      */
     double thr_hi;       /* p -= 1 if S > thr_hi * gamma_t * C2 (paper: 1.3)      */
+    int64_t sync_warmup_steps; /* steps t < this sync after every step with no controller
+                                  update (the paper's p = 1 warm-up, Sec. III-B, IV-C);
+                                  Algorithm 2 then starts with cnt = 0, p = p_init; 0 = none */
+    int64_t p_switch_step;     /* constant mode: from step p_switch_step on, the period is
+                                  p_after (Sec. III-A strategies, the decreasing-period
+                                  baseline of Sec. V-B); 0 = never                           */
+    int32_t p_after;           /* the period after p_switch_step, >= 1 when used            */
+    int32_t avg_momentum;      /* 1: a sync also replaces every momentum buffer by the mean
+                                  of the K buffers; 0: momentum stays local (default)        */
 } adpsgd_hparams;
 
 /* Caller-owned device memory, on the device current at adpsgd_init. */
@@ -159,14 +174,15 @@ ADPSGD_API int adpsgd_average(adpsgd_ctx *c, double *var_out);
 ADPSGD_API int adpsgd_step_average(adpsgd_ctx *c, double *var_out);
 
 /* Period controller (Algorithm 2, lines 13-19) for a sync after step t - 1 with
- * S = sum(var[0..T)).  Sampling phase (t-1 < k_s): C2 <- running mean of
- * S / gamma; otherwise p + 1 if S < thr_lo gamma C2, p - 1 if S > thr_hi
- * gamma C2.  Constant mode: no change.  *next_period (may be NULL) receives p.
- * ENONFINITE, with the state unchanged, if S is NaN or infinite. */
+ * S = sum(var[0..T)), as adpsgd_sched_on_sync.  Sampling phase (t-1 < k_s):
+ * C2 <- running mean of S / gamma; otherwise p + 1 if S < thr_lo gamma C2,
+ * p - 1 if S > thr_hi gamma C2.  Constant mode and the warm-up prefix: no
+ * change.  *next_period (may be NULL) receives p.  ENONFINITE, with the state
+ * unchanged, if S is NaN or infinite. */
 ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_period);
 
 /* Run n_steps steps of Algorithm 2 from the current state: local steps, a sync
- * whenever cnt reaches p (fused into that period's last step), and the
+ * whenever adpsgd_sched_step says one is due (fused into that step), and the
  * controller after every sync.  log (host, log_cap records) and var_log (host,
  * [log_cap][T], may be NULL) receive the first log_cap syncs; *n_syncs (may be
  * NULL) the count of all syncs.  No sync is forced at the end.  Returns when
@@ -215,10 +231,18 @@ ADPSGD_API double adpsgd_lr(const adpsgd_hparams *hp, int64_t t);
 /* Initial controller state: t = cnt = nC2 = 0, C2 = 0, p = p_init. */
 ADPSGD_API int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st);
 
-/* Apply Algorithm 2, lines 13-19, for a sync after step t with variance S;
- * *margin (may be NULL) receives the decision margin (NaN if no decision).
- * Updates st->p, st->C2, st->nC2 only.  ENONFINITE (state unchanged) if S is
- * not finite; EINVAL on a NULL pointer. */
+/* Begin step t = st->t (Algorithm 2, line 5, and the test of line 8): cnt += 1,
+ * the period in force is set (p_after from p_switch_step on, constant modes),
+ * and *sync_due = 1 if a sync follows this step: always during the warm-up
+ * prefix, t mod p == 0 in ADPSGD_PERIOD_ALG1, cnt >= p otherwise.  Advances
+ * st->t.  EINVAL on a NULL pointer. */
+ADPSGD_API int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int32_t *sync_due);
+
+/* Apply Algorithm 2, lines 9 and 13-19, for a sync after step t with variance
+ * S: cnt = 0; in adaptive mode after the warm-up prefix, C2 sampling (t < k_s)
+ * or p +- 1.  *margin (may be NULL) receives the decision margin (NaN if no
+ * decision).  ENONFINITE (state unchanged) if S is not finite; EINVAL on a
+ * NULL pointer. */
 ADPSGD_API int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
                          double *margin);
 

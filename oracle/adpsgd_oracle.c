@@ -135,13 +135,18 @@ typedef struct {
     const int64_t *offsets;    /* [T+1], offsets[0] = 0, offsets[T] = P */
     uint64_t seed;
     double sigma, momentum, weight_decay, h_lo, h_hi;
-    int32_t lr_kind;           /* 0 constant, 1 step decay, 2 cosine */
-    int32_t period_mode;       /* 0 constant period, 1 adaptive (Algorithm 2) */
+    int32_t lr_kind;           /* 0 constant, 1 step decay, 2 cosine, 3 gradual warm-up + steps */
+    int32_t period_mode;       /* 0 constant period, 1 adaptive (Algorithm 2),
+                                  2 constant period with Algorithm 1's test (k mod p == 0) */
     double lr0;
     int64_t total_steps;
     int64_t k_s;
     double thr_lo, thr_hi;
     int32_t p_init;
+    int32_t avg_momentum;      /* 1: a sync averages the momentum buffers too */
+    int64_t sync_warmup_steps; /* steps before this one sync every step, no controller */
+    int64_t p_switch_step;     /* constant modes: period p_after from this step on (0: never) */
+    int32_t p_after;
     int32_t pad_;
 } orc_problem;
 
@@ -165,7 +170,10 @@ typedef struct {
 
 /* Learning rate of 0-based step t.  Step decay: x0.1 at floor(N/2) and again
  * at floor(3N/4) (the paper decays by 10x at 1/2 and 3/4 of training,
- * Section IV-B); cosine: lr0 * (1 + cos(pi t / N)) / 2. */
+ * Section IV-B); cosine: lr0 * (1 + cos(pi t / N)) / 2.  Gradual warm-up
+ * (Section IV-C: 90 epochs; the rate starts at lr0 and grows by lr0 each epoch
+ * for 8 epochs, stays at 8 lr0, and is cut by 10x at epochs 30 and 60), with
+ * an epoch of E = floor(N / 90) steps (at least one). */
 double orc_lr(const orc_problem *pb, int64_t t)
 {
     double N = (double)pb->total_steps;
@@ -178,6 +186,16 @@ double orc_lr(const orc_problem *pb, int64_t t)
     }
     case 2:
         return pb->lr0 * 0.5 * (1.0 + cos(ORC_PI * (double)t / N));
+    case 3: {
+        int64_t E = pb->total_steps / 90;
+        if (E < 1) E = 1;
+        int64_t epoch = t / E;
+        if (epoch < 8) return pb->lr0 * (double)(epoch + 1);
+        double g = 8.0 * pb->lr0;
+        if (epoch >= 30) g *= 0.1;
+        if (epoch >= 60) g *= 0.1;
+        return g;
+    }
     default:
         return pb->lr0;
     }
@@ -251,11 +269,22 @@ static void tensor_range(const orc_problem *pb, const int64_t *idx, int64_t n, i
 /* The synchronization step (Algorithm 2, lines 10-12):
  *   xbar_i  = (1/K) sum_k x_{k,i}
  *   var_tau = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2      (pre-average x)
- *   x_{k,i} = xbar_i for every k; momentum untouched.
+ *   x_{k,i} = xbar_i for every k; momentum untouched unless avg_momentum, in
+ *   which case v_{k,i} = (1/K) sum_j v_{j,i} as well (v may then not be NULL).
  * S = sum_tau var_tau is the paper's S_k (Var[.] of Section II-B with the squared
  * norm).  Returns S; var_out[T] receives the per-tensor terms. */
-double orc_average(const orc_problem *pb, const int64_t *idx, int64_t n, double *x, double *var_out)
+double orc_average(const orc_problem *pb, const int64_t *idx, int64_t n, double *x, double *v,
+                   double *var_out)
 {
+    if (pb->avg_momentum && v) {
+#pragma omp parallel for schedule(static)
+        for (int64_t j = 0; j < n; ++j) {
+            double s = 0.0;
+            for (int32_t k = 0; k < pb->K; ++k) s += v[(int64_t)k * n + j];
+            double vbar = s / (double)pb->K;
+            for (int32_t k = 0; k < pb->K; ++k) v[(int64_t)k * n + j] = vbar;
+        }
+    }
     const int32_t K = pb->K;
     double *xbar = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
 #pragma omp parallel for schedule(static)
@@ -286,11 +315,13 @@ double orc_average(const orc_problem *pb, const int64_t *idx, int64_t n, double 
 }
 
 /* Period controller after a sync at step t with variance S (Algorithm 2,
- * lines 13-19).  Returns 0, or -4 if S is not finite (state unchanged). */
+ * lines 13-19).  Inactive in the constant modes and during the warm-up prefix
+ * (there the run synchronizes every step and Algorithm 2 has not started).
+ * Returns 0, or -4 if S is not finite (state unchanged). */
 int orc_controller(const orc_problem *pb, orc_state *st, int64_t t, double S)
 {
     if (!isfinite(S)) return -4;
-    if (pb->period_mode != 1) return 0;
+    if (pb->period_mode != 1 || t < pb->sync_warmup_steps) return 0;
     double gamma = orc_lr(pb, t);
     if (t < pb->k_s) {
         /* sampling phase: running (cumulative) mean of S / gamma */
@@ -310,6 +341,41 @@ void orc_state_init(const orc_problem *pb, orc_state *st)
     st->p = pb->p_init;
 }
 
+/* Start of step t: count it (Algorithm 2, line 5), apply the two-phase
+ * constant period (Section III-A strategies, Section V-B), and say whether a
+ * sync follows it: every step of the p = 1 warm-up prefix (Sections III-B,
+ * IV-C); t mod p == 0 under Algorithm 1's test; cnt == p under Algorithm 2's
+ * (line 8; written >= so a period that shrinks under the counter still ends). */
+static int begin_step(const orc_problem *pb, orc_state *st, int64_t t)
+{
+    st->cnt += 1;
+    if (pb->period_mode != 1 && pb->p_switch_step > 0 && t >= pb->p_switch_step) st->p = pb->p_after;
+    if (t < pb->sync_warmup_steps) return 1;
+    if (pb->period_mode == 2) return (t % st->p) == 0;
+    return st->cnt >= st->p;
+}
+
+/* The schedule alone, driven by scripted variances: S_by_step[t] is taken as
+ * the variance of a sync after step t.  Records the sync steps and the period
+ * in force for each (up to cap); returns the sync count or -4 on a non-finite S. */
+int64_t orc_schedule_trace(const orc_problem *pb, orc_state *st, int64_t n_steps,
+                           const double *S_by_step, int64_t *sync_t, int32_t *sync_p, int64_t cap)
+{
+    int64_t n_sync = 0;
+    for (int64_t s = 0; s < n_steps; ++s) {
+        int64_t t = st->t;
+        int sync = begin_step(pb, st, t);
+        st->t = t + 1;
+        if (!sync) continue;
+        st->cnt = 0;
+        if (n_sync < cap) { sync_t[n_sync] = t; sync_p[n_sync] = st->p; }
+        n_sync += 1;
+        int rc = orc_controller(pb, st, t, S_by_step[t]);
+        if (rc) return rc;
+    }
+    return n_sync;
+}
+
 /* Run steps st->t .. st->t + n_steps - 1 of Algorithm 2 on the selection idx
  * (idx NULL: all P elements; a strict subset is allowed only with a constant
  * period, where the sync schedule does not depend on the data).
@@ -325,11 +391,11 @@ int64_t orc_run(const orc_problem *pb, const int64_t *idx, int64_t n, orc_state 
     int64_t n_sync = 0;
     for (int64_t s = 0; s < n_steps; ++s) {
         int64_t t = st->t;
-        st->cnt += 1;
+        int sync = begin_step(pb, st, t);
         orc_local_step(pb, idx, n, t, h, xs, x, v);
-        if (st->cnt == st->p) {
+        if (sync) {
             st->cnt = 0;
-            double S = orc_average(pb, idx, n, x, var);
+            double S = orc_average(pb, idx, n, x, v, var);
             int32_t p_used = st->p;
             int rc = orc_controller(pb, st, t, S);
             if (n_sync < log_cap) {
@@ -349,7 +415,8 @@ int64_t orc_run(const orc_problem *pb, const int64_t *idx, int64_t n, orc_state 
 }
 
 /* The replica mean under any sync schedule.  Syncs replace each x_k by the mean
- * and leave v alone, so they preserve both means; the dynamics are affine in
+ * and leave v alone (or replace it by its mean), so they preserve both means;
+ * the dynamics are affine in
  * (x, v), so the means follow one momentum-SGD run driven by the K-averaged
  * noise: zbar = (1/K) sum_k z_k.  xbar, vbar: [n], updated in place. */
 void orc_mean_trajectory(const orc_problem *pb, const int64_t *idx, int64_t n, int64_t t0,

@@ -45,7 +45,9 @@ class _Problem(C.Structure):
         ("lr_kind", C.c_int32), ("period_mode", C.c_int32),
         ("lr0", C.c_double), ("total_steps", C.c_int64), ("k_s", C.c_int64),
         ("thr_lo", C.c_double), ("thr_hi", C.c_double),
-        ("p_init", C.c_int32), ("pad_", C.c_int32),
+        ("p_init", C.c_int32), ("avg_momentum", C.c_int32),
+        ("sync_warmup_steps", C.c_int64), ("p_switch_step", C.c_int64),
+        ("p_after", C.c_int32), ("pad_", C.c_int32),
     ]
 
 
@@ -78,8 +80,11 @@ def _load():
         lib.orc_lr.restype = C.c_double
         lib.orc_problem_data.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, _D, _D]
         lib.orc_local_step.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, C.c_int64, _D, _D, _D, _D]
-        lib.orc_average.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, _D, _D]
+        lib.orc_average.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, _D, _D, _D]
         lib.orc_average.restype = C.c_double
+        lib.orc_schedule_trace.argtypes = [C.POINTER(_Problem), C.POINTER(_State), C.c_int64, _D,
+                                           _I64, C.POINTER(C.c_int32), C.c_int64]
+        lib.orc_schedule_trace.restype = C.c_int64
         lib.orc_controller.argtypes = [C.POINTER(_Problem), C.POINTER(_State), C.c_int64, C.c_double]
         lib.orc_controller.restype = C.c_int
         lib.orc_state_init.argtypes = [C.POINTER(_Problem), C.POINTER(_State)]
@@ -162,7 +167,9 @@ class Oracle:
             sigma=w.sigma, momentum=w.momentum, weight_decay=w.weight_decay,
             h_lo=w.h_lo, h_hi=w.h_hi, lr_kind=w.lr_kind, period_mode=w.period_mode,
             lr0=w.lr0, total_steps=w.total_steps, k_s=w.k_s, thr_lo=w.thr_lo,
-            thr_hi=w.thr_hi, p_init=w.p_init, pad_=0)
+            thr_hi=w.thr_hi, p_init=w.p_init, avg_momentum=1 if w.avg_momentum else 0,
+            sync_warmup_steps=w.sync_warmup_steps, p_switch_step=w.p_switch_step,
+            p_after=w.p_after, pad_=0)
         self.lib = _load()
 
     def lr(self, t: int) -> float:
@@ -178,9 +185,10 @@ class Oracle:
         n = x.shape[1]
         self.lib.orc_local_step(C.byref(self.pb), _ip(idx), n, t, _dp(h), _dp(xs), _dp(x), _dp(v))
 
-    def average(self, x, idx=None):
+    def average(self, x, idx=None, v=None):
+        """Sync x (and v when the workload averages momentum); returns (S, var[T])."""
         var = np.zeros(self.w.T)
-        S = self.lib.orc_average(C.byref(self.pb), _ip(idx), x.shape[1], _dp(x), _dp(var))
+        S = self.lib.orc_average(C.byref(self.pb), _ip(idx), x.shape[1], _dp(x), _dp(v), _dp(var))
         return float(S), var
 
     def new_state(self):
@@ -258,22 +266,20 @@ def lr(w, t: int) -> float:
     return Oracle(w).lr(t)
 
 
-def controller_trace(w, S_of_sync, sync_steps=None):
-    """Drive the oracle controller with a scripted sequence of S values.
+def controller_trace(w, S_of_sync):
+    """Drive the oracle's schedule with scripted variances.
 
     S_of_sync(t, gamma) gives S for a sync after step t.  Returns the list of
-    (t, p_used) syncs over w.total_steps steps, following Algorithm 2's counter.
+    (t, p in force) syncs over w.total_steps steps and the final state.
     """
     o = Oracle(w)
     st = o.new_state()
-    out = []
-    for t in range(w.total_steps):
-        st.cnt += 1
-        if st.cnt == st.p:
-            st.cnt = 0
-            p_used = st.p
-            rc = o.controller(st, t, float(S_of_sync(t, o.lr(t))))
-            out.append((t, p_used))
-            if rc:
-                raise FloatingPointError(rc)
-    return out, st
+    N = w.total_steps
+    S = np.array([float(S_of_sync(t, o.lr(t))) for t in range(N)])
+    sync_t = np.zeros(N, dtype=np.int64)
+    sync_p = np.zeros(N, dtype=np.int32)
+    n = o.lib.orc_schedule_trace(C.byref(o.pb), C.byref(st), N, _dp(S), _ip(sync_t),
+                                 sync_p.ctypes.data_as(C.POINTER(C.c_int32)), N)
+    if n < 0:
+        raise FloatingPointError(n)
+    return [(int(a), int(b)) for a, b in zip(sync_t[:n], sync_p[:n])], st

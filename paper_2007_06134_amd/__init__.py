@@ -12,10 +12,10 @@ import numpy as np
 
 from ._native import (  # noqa: F401
     AdpsgdError, EDEVICE, EINVAL, ENONFINITE, ESTATE, EXPORTED, LIB_PATH, LR_CONST, LR_COSINE,
-    LR_STEP, OK, PERIOD_ADAPTIVE, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
+    LR_STEP, LR_WARMUP_STEP, OK, PERIOD_ADAPTIVE, PERIOD_ALG1, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
     adpsgd_get_state, adpsgd_get_timing, adpsgd_hparams, adpsgd_init, adpsgd_last_error,
     adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,
-    adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_schedule, adpsgd_set_state, adpsgd_set_timing,
+    adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_state, adpsgd_set_timing,
     adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
     make_hparams,
 )
@@ -26,7 +26,10 @@ def hparams_of(w) -> adpsgd_hparams:
     return make_hparams(seed=w.seed, sigma=w.sigma, momentum=w.momentum, weight_decay=w.weight_decay,
                         h_lo=w.h_lo, h_hi=w.h_hi, lr_kind=w.lr_kind, lr0=w.lr0,
                         total_steps=w.total_steps, period_mode=w.period_mode, p_init=w.p_init,
-                        k_s=w.k_s, thr_lo=w.thr_lo, thr_hi=w.thr_hi)
+                        k_s=w.k_s, thr_lo=w.thr_lo, thr_hi=w.thr_hi,
+                        sync_warmup_steps=getattr(w, "sync_warmup_steps", 0),
+                        p_switch_step=getattr(w, "p_switch_step", 0), p_after=getattr(w, "p_after", 0),
+                        avg_momentum=getattr(w, "avg_momentum", False))
 
 
 class Adpsgd:

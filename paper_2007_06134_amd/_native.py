@@ -17,8 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libadpsgd.so")
 
 OK, EINVAL, ESTATE, EDEVICE, ENONFINITE = 0, -1, -2, -3, -4
-LR_CONST, LR_STEP, LR_COSINE = 0, 1, 2
-PERIOD_CONST, PERIOD_ADAPTIVE = 0, 1
+LR_CONST, LR_STEP, LR_COSINE, LR_WARMUP_STEP = 0, 1, 2, 3
+PERIOD_CONST, PERIOD_ADAPTIVE, PERIOD_ALG1 = 0, 1, 2
 
 
 class AdpsgdError(RuntimeError):
@@ -34,6 +34,8 @@ class adpsgd_hparams(C.Structure):
         ("lr_kind", C.c_int32), ("period_mode", C.c_int32), ("lr0", C.c_double),
         ("total_steps", C.c_int64), ("p_init", C.c_int32), ("p_max", C.c_int32),
         ("k_s", C.c_int64), ("thr_lo", C.c_double), ("thr_hi", C.c_double),
+        ("sync_warmup_steps", C.c_int64), ("p_switch_step", C.c_int64), ("p_after", C.c_int32),
+        ("avg_momentum", C.c_int32),
     ]
 
 
@@ -92,6 +94,7 @@ _SIGS = {
                                      C.c_int64, C.c_void_p, C.c_void_p]),
     "adpsgd_lr": (C.c_double, [C.POINTER(adpsgd_hparams), C.c_int64]),
     "adpsgd_sched_init": (C.c_int, [C.POINTER(adpsgd_hparams), C.POINTER(adpsgd_state)]),
+    "adpsgd_sched_step": (C.c_int, [C.POINTER(adpsgd_hparams), C.POINTER(adpsgd_state), C.POINTER(C.c_int32)]),
     "adpsgd_sched_on_sync": (C.c_int, [C.POINTER(adpsgd_hparams), C.POINTER(adpsgd_state), C.c_int64,
                                        C.c_double, _DP]),
 }
@@ -118,11 +121,14 @@ def adpsgd_last_error() -> str:
 
 
 def make_hparams(seed, sigma, momentum, weight_decay, h_lo, h_hi, lr_kind, lr0, total_steps,
-                 period_mode, p_init, k_s, thr_lo=0.7, thr_hi=1.3, p_max=0) -> adpsgd_hparams:
+                 period_mode, p_init, k_s, thr_lo=0.7, thr_hi=1.3, p_max=0, sync_warmup_steps=0,
+                 p_switch_step=0, p_after=0, avg_momentum=False) -> adpsgd_hparams:
     return adpsgd_hparams(seed=seed, sigma=sigma, momentum=momentum, weight_decay=weight_decay,
                           h_lo=h_lo, h_hi=h_hi, lr_kind=lr_kind, period_mode=period_mode, lr0=lr0,
                           total_steps=total_steps, p_init=p_init, p_max=p_max, k_s=k_s,
-                          thr_lo=thr_lo, thr_hi=thr_hi)
+                          thr_lo=thr_lo, thr_hi=thr_hi, sync_warmup_steps=sync_warmup_steps,
+                          p_switch_step=p_switch_step, p_after=p_after,
+                          avg_momentum=1 if avg_momentum else 0)
 
 
 def adpsgd_workspace_bytes(K: int, P: int, offsets: Sequence[int]) -> int:
@@ -224,6 +230,13 @@ def adpsgd_sched_init(hp: adpsgd_hparams) -> adpsgd_state:
     st = adpsgd_state()
     _check(lib.adpsgd_sched_init(C.byref(hp), C.byref(st)))
     return st
+
+
+def adpsgd_sched_step(hp: adpsgd_hparams, st: adpsgd_state) -> bool:
+    """Begins step st.t (updates st in place); True if a sync follows it."""
+    due = C.c_int32()
+    _check(lib.adpsgd_sched_step(C.byref(hp), C.byref(st), C.byref(due)))
+    return bool(due.value)
 
 
 def adpsgd_sched_on_sync(hp: adpsgd_hparams, st: adpsgd_state, t: int, S: float) -> float:

@@ -1,6 +1,7 @@
 // Host-only parts of ADPSGD: the learning-rate schedules and the adaptive
 // period controller (Algorithm 2, lines 1-3 and 13-19).  No HIP here, so the
 // controller runs and is tested without a GPU.
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <limits>
@@ -17,8 +18,9 @@ bool hparams_valid(const adpsgd_hparams *hp, std::string *why) {
     if (!(hp->momentum >= 0 && hp->momentum < 1)) return bad("momentum must be in [0, 1)");
     if (!(std::isfinite(hp->weight_decay) && hp->weight_decay >= 0)) return bad("weight_decay must be finite and >= 0");
     if (!(hp->h_lo > 0 && hp->h_lo <= hp->h_hi && std::isfinite(hp->h_hi))) return bad("need 0 < h_lo <= h_hi < inf");
-    if (hp->lr_kind < ADPSGD_LR_CONST || hp->lr_kind > ADPSGD_LR_COSINE) return bad("unknown lr_kind");
-    if (hp->period_mode != ADPSGD_PERIOD_CONST && hp->period_mode != ADPSGD_PERIOD_ADAPTIVE)
+    if (hp->lr_kind < ADPSGD_LR_CONST) return bad("unknown lr_kind");
+    if (hp->period_mode != ADPSGD_PERIOD_CONST && hp->period_mode != ADPSGD_PERIOD_ADAPTIVE &&
+        hp->period_mode != ADPSGD_PERIOD_ALG1)
         return bad("unknown period_mode");
     if (!(std::isfinite(hp->lr0) && hp->lr0 > 0)) return bad("lr0 must be finite and > 0");
     if (hp->total_steps < 1) return bad("total_steps must be >= 1");
@@ -27,6 +29,14 @@ bool hparams_valid(const adpsgd_hparams *hp, std::string *why) {
     if (hp->k_s < 0) return bad("k_s must be >= 0");
     if (!(std::isfinite(hp->thr_lo) && std::isfinite(hp->thr_hi) && hp->thr_lo > 0 && hp->thr_lo <= hp->thr_hi))
         return bad("need 0 < thr_lo <= thr_hi");
+    if (hp->lr_kind > ADPSGD_LR_WARMUP_STEP) return bad("unknown lr_kind");
+    if (hp->sync_warmup_steps < 0) return bad("sync_warmup_steps must be >= 0");
+    if (hp->p_switch_step < 0) return bad("p_switch_step must be >= 0");
+    if (hp->p_switch_step > 0 && hp->period_mode == ADPSGD_PERIOD_ADAPTIVE)
+        return bad("p_switch_step applies to the constant period modes only");
+    if (hp->p_switch_step > 0 && (hp->p_after < 1 || (hp->p_max > 0 && hp->p_after > hp->p_max)))
+        return bad("p_after must be in [1, p_max] when p_switch_step is set");
+    if (hp->avg_momentum != 0 && hp->avg_momentum != 1) return bad("avg_momentum must be 0 or 1");
     return true;
 }
 
@@ -48,6 +58,16 @@ extern "C" double adpsgd_lr(const adpsgd_hparams *hp, int64_t t) {
     }
     case ADPSGD_LR_COSINE:
         return 0.5 * hp->lr0 * (1.0 + std::cos(M_PI * (double)t / (double)hp->total_steps));
+    case ADPSGD_LR_WARMUP_STEP: {
+        // 90 "epochs" of E steps: a linear ramp over the first 8 (lr0, 2 lr0, ...,
+        // 8 lr0), then 8 lr0 with 10x decays at epochs 30 and 60
+        const int64_t E = std::max<int64_t>(1, hp->total_steps / 90);
+        if (t < 8 * E) return hp->lr0 * (double)(1 + t / E);
+        double g = 8.0 * hp->lr0;
+        if (t >= 30 * E) g *= 0.1;
+        if (t >= 60 * E) g *= 0.1;
+        return g;
+    }
     default:
         return hp->lr0;
     }
@@ -62,12 +82,26 @@ extern "C" int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st) {
     return ok();
 }
 
+extern "C" int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int32_t *sync_due) {
+    if (!hp || !st || !sync_due) return fail(ADPSGD_EINVAL, "NULL hparams, state or output");
+    const int64_t t = st->t;
+    st->cnt += 1;
+    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE && hp->p_switch_step > 0 && t >= hp->p_switch_step)
+        st->p = hp->p_after;
+    if (t < hp->sync_warmup_steps) *sync_due = 1;
+    else if (hp->period_mode == ADPSGD_PERIOD_ALG1) *sync_due = (t % st->p) == 0;
+    else *sync_due = st->cnt >= st->p;
+    st->t = t + 1;
+    return ok();
+}
+
 extern "C" int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
                                     double *margin) {
     if (!hp || !st) return fail(ADPSGD_EINVAL, "NULL hparams or state");
     if (margin) *margin = std::numeric_limits<double>::quiet_NaN();
     if (!std::isfinite(S)) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
-    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE) return ok();
+    st->cnt = 0;
+    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE || t < hp->sync_warmup_steps) return ok();
     const double gamma = adpsgd_lr(hp, t);
     if (t < hp->k_s) {
         // sampling phase: C2 is the running (cumulative) mean of S / gamma

@@ -158,12 +158,14 @@ __device__ __forceinline__ f4 tree_sum_lds(const f4 (*rows)[64], int lane, int b
 // thread steps its rows (if fused), publishes them in LDS, reads all K rows of
 // its lane back to form the mean in a fixed order (the same bits in every
 // thread), then writes the mean over its rows and sums its squared deviations.
-// Lanes of groups cut by the tile bounds use masked scalar accesses.
-template <int KT, bool VEC, bool NT, bool FUSED>
+// AVGM also replaces the momentum rows by their mean, the same way.  Lanes of
+// groups cut by the tile bounds use masked scalar accesses.
+template <int KT, bool VEC, bool NT, bool FUSED, bool AVGM>
 __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParams p) {
     constexpr int W = KT < 16 ? KT : 16;
     constexpr int R = KT / W;
     __shared__ f4 rows[KT][64];
+    __shared__ f4 mrows[AVGM ? KT : 1][64];
     const StepParams &a = p.s;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const Tile tile = p.tiles[blockIdx.x];
@@ -180,7 +182,7 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
         for (int r = 0; r < R; ++r) {
             float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
             xr[r] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
-            if (FUSED) {
+            if (FUSED || AVGM) {
                 float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
                 m[r] = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
             }
@@ -192,12 +194,17 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
             for (int r = 0; r < R; ++r) {
                 const int k = w + W * r;
                 sgd_update(a, xr[r], m[r], h, xs, step_noise(a, g, k));
-                float *mrow = a.m + (int64_t)k * a.P + e0;
-                if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
+                if (!AVGM) {
+                    float *mrow = a.m + (int64_t)k * a.P + e0;
+                    if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
+                }
             }
         }
 #pragma unroll
-        for (int r = 0; r < R; ++r) rows[w + W * r][lane] = xr[r];
+        for (int r = 0; r < R; ++r) {
+            rows[w + W * r][lane] = xr[r];
+            if (AVGM) mrows[w + W * r][lane] = m[r];
+        }
     }
     __syncthreads();
     double acc = 0.0;
@@ -211,6 +218,14 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
             float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
             if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
         }
+        if (AVGM) {
+            const f4 mmean = tree_sum_lds<KT>(mrows, lane, 0) / splat((float)KT);
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
+                if (full) st4<NT>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
+            }
+        }
         if (!full) dev2 = mask4(dev2, e0, lo, hi);
         acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
     }
@@ -220,8 +235,9 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
 
 // Any K: one wave per tile, lane = group, the workers walked in a loop.  The
 // first pass sums the replicas (stepping and storing them if fused), the
-// second re-reads them for the deviations and writes the mean.
-template <bool VEC, bool FUSED>
+// second re-reads them for the deviations and writes the mean.  AVGM sums the
+// momentum buffers in the first pass and writes their mean in the second.
+template <bool VEC, bool FUSED, bool AVGM>
 __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     const StepParams &a = p.s;
     const Tile tile = p.tiles[blockIdx.x];
@@ -236,20 +252,23 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             if (full) { h = ld4<false>(a.h + e0); xs = ld4<false>(a.xs + e0); }
             else { h = ld4_masked(a.h + e0, e0, lo, hi); xs = ld4_masked(a.xs + e0, e0, lo, hi); }
         }
-        f4 s = splat(0.0f);
+        f4 s = splat(0.0f), sm = splat(0.0f);
         for (int k = 0; k < a.K; ++k) {
             float *xrow = a.x + (int64_t)k * a.P + e0;
+            float *mrow = a.m + (int64_t)k * a.P + e0;
             f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
+            f4 m = splat(0.0f);
+            if (FUSED || AVGM) m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
             if (FUSED) {
-                float *mrow = a.m + (int64_t)k * a.P + e0;
-                f4 m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
                 sgd_update(a, x, m, h, xs, step_noise(a, g, k));
-                if (full) { st4<false>(mrow, m); st4<false>(xrow, x); }
-                else { st4_masked(mrow, m, e0, lo, hi); st4_masked(xrow, x, e0, lo, hi); }
+                if (full) st4<false>(xrow, x); else st4_masked(xrow, x, e0, lo, hi);
+                if (!AVGM) { if (full) st4<false>(mrow, m); else st4_masked(mrow, m, e0, lo, hi); }
             }
             s = (k == 0) ? x : s + x;
+            if (AVGM) sm = (k == 0) ? m : sm + m;
         }
         const f4 mean = s / splat((float)a.K);
+        const f4 mmean = sm / splat((float)a.K);
         f4 dev2 = splat(0.0f);
         for (int k = 0; k < a.K; ++k) {
             float *xrow = a.x + (int64_t)k * a.P + e0;
@@ -257,6 +276,10 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             const f4 dk = mean - x;
             dev2 = fma4(dk, dk, dev2);
             if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
+            if (AVGM) {
+                float *mrow = a.m + (int64_t)k * a.P + e0;
+                if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
+            }
         }
         if (!full) dev2 = mask4(dev2, e0, lo, hi);
         acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
@@ -320,19 +343,30 @@ __global__ void __launch_bounds__(kBlock) k_normal_dump(RoundKeys rk, uint32_t c
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
 
-template <int KT>
-hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt, hipStream_t st) {
+template <int KT, bool FUSED, bool AVGM>
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, hipStream_t st) {
     constexpr int threads = 64 * (KT < 16 ? KT : 16);
     const dim3 grid((unsigned)n_tiles), block(threads);
-    if (fused) {
-        if (vec && nt) k_sync_lds<KT, true, true, true><<<grid, block, 0, st>>>(p);
-        else if (vec) k_sync_lds<KT, true, false, true><<<grid, block, 0, st>>>(p);
-        else k_sync_lds<KT, false, false, true><<<grid, block, 0, st>>>(p);
-    } else {
-        if (vec && nt) k_sync_lds<KT, true, true, false><<<grid, block, 0, st>>>(p);
-        else if (vec) k_sync_lds<KT, true, false, false><<<grid, block, 0, st>>>(p);
-        else k_sync_lds<KT, false, false, false><<<grid, block, 0, st>>>(p);
-    }
+    if (vec && nt) k_sync_lds<KT, true, true, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    else if (vec) k_sync_lds<KT, true, false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    else k_sync_lds<KT, false, false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    return hipGetLastError();
+}
+
+template <int KT>
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec, bool nt,
+                         hipStream_t st) {
+    if (fused && avg_m) return sync_dispatch<KT, true, true>(p, n_tiles, vec, nt, st);
+    if (fused) return sync_dispatch<KT, true, false>(p, n_tiles, vec, nt, st);
+    if (avg_m) return sync_dispatch<KT, false, true>(p, n_tiles, vec, nt, st);
+    return sync_dispatch<KT, false, false>(p, n_tiles, vec, nt, st);
+}
+
+template <bool FUSED, bool AVGM>
+hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, hipStream_t st) {
+    const dim3 grid((unsigned)n_tiles), block(64);
+    if (vec) k_sync_loop<true, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    else k_sync_loop<false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
     return hipGetLastError();
 }
 
@@ -352,26 +386,21 @@ hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool vec, bool nt, hipStream_t st) {
+hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec, bool nt,
+                            hipStream_t st) {
     if (n_tiles <= 0) return hipSuccess;
     switch (p.s.K) {
-    case 1: return sync_dispatch<1>(p, n_tiles, fused, vec, nt, st);
-    case 2: return sync_dispatch<2>(p, n_tiles, fused, vec, nt, st);
-    case 4: return sync_dispatch<4>(p, n_tiles, fused, vec, nt, st);
-    case 8: return sync_dispatch<8>(p, n_tiles, fused, vec, nt, st);
-    case 16: return sync_dispatch<16>(p, n_tiles, fused, vec, nt, st);
-    case 32: return sync_dispatch<32>(p, n_tiles, fused, vec, nt, st);
-    default: {
-        const dim3 grid((unsigned)n_tiles), block(64);
-        if (fused) {
-            if (vec) k_sync_loop<true, true><<<grid, block, 0, st>>>(p);
-            else k_sync_loop<false, true><<<grid, block, 0, st>>>(p);
-        } else {
-            if (vec) k_sync_loop<true, false><<<grid, block, 0, st>>>(p);
-            else k_sync_loop<false, false><<<grid, block, 0, st>>>(p);
-        }
-        return hipGetLastError();
-    }
+    case 1: return sync_dispatch<1>(p, n_tiles, fused, avg_m, vec, nt, st);
+    case 2: return sync_dispatch<2>(p, n_tiles, fused, avg_m, vec, nt, st);
+    case 4: return sync_dispatch<4>(p, n_tiles, fused, avg_m, vec, nt, st);
+    case 8: return sync_dispatch<8>(p, n_tiles, fused, avg_m, vec, nt, st);
+    case 16: return sync_dispatch<16>(p, n_tiles, fused, avg_m, vec, nt, st);
+    case 32: return sync_dispatch<32>(p, n_tiles, fused, avg_m, vec, nt, st);
+    default:
+        if (fused && avg_m) return loop_dispatch<true, true>(p, n_tiles, vec, st);
+        if (fused) return loop_dispatch<true, false>(p, n_tiles, vec, st);
+        if (avg_m) return loop_dispatch<false, true>(p, n_tiles, vec, st);
+        return loop_dispatch<false, false>(p, n_tiles, vec, st);
     }
 }
 

@@ -49,8 +49,9 @@ struct SyncParams {
 int64_t local_step_blocks(int64_t n_groups, int32_t K);
 // vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4.
 hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, hipStream_t st);
-// fused = true: the local step and the sync in one pass.
-hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool vec,
+// fused = true: the local step and the sync in one pass.  avg_m = true: the
+// momentum buffers are averaged as well.
+hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec,
                             bool nontemporal, hipStream_t st);
 // chunk_partials[c] = sum of the tile partials of chunk c; then
 // var[tau] = (sum of the partials of tau's chunks) / K, where tau's chunks are

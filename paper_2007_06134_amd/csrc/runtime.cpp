@@ -271,7 +271,7 @@ int enqueue_sync(adpsgd_ctx *c, bool fused, int64_t t, int slot) {
     sp.partials = c->d_tile_partials;
     const int64_t n_tiles = (int64_t)c->tiles.size();
     int rc = timed_launch(c, fused ? kFused : kAverage, [&] {
-        return launch_tile_sync(sp, n_tiles, fused, c->vec, c->nontemporal, c->stream);
+        return launch_tile_sync(sp, n_tiles, fused, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream);
     });
     if (rc) return rc;
     double *dv = c->d_var + (size_t)slot * c->T;
@@ -446,42 +446,41 @@ extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, 
     const adpsgd_hparams &hp = c->hp;
     const bool adaptive = hp.period_mode == ADPSGD_PERIOD_ADAPTIVE;
     const int64_t end = c->st.t + n_steps;
-    // Enqueue side: t_enq/cnt_enq track what is on the stream.  c->st (p, C2)
-    // is the controller's view, advanced as syncs are read back in order.
-    int64_t t_enq = c->st.t, cnt_enq = c->st.cnt;
-    int32_t p_known = c->st.p;
+    // plan: the schedule as enqueued on the stream (t, cnt, p).  c->st: the
+    // controller's view (p, C2, nC2), advanced as syncs are read back in order.
+    // They differ only while a decisive sync (one whose decision may move p) is
+    // in flight; then only steps that end no period under p - 1, p or p + 1
+    // are enqueued, so the GPU keeps working while the host waits.
+    adpsgd_state plan = c->st;
     struct Pending { int64_t t; int32_t p; int slot; bool decisive; };
     std::deque<Pending> pend;
-    int64_t n_enq_syncs = 0, n_done = 0;
-    bool blocked = false;   // a sync whose decision sets the next period is in flight
+    int64_t n_enq_syncs = 0, n_done = 0, lookahead = 0;
+    bool blocked = false;
     int status = ADPSGD_OK;
 
     while (true) {
-        while (status == ADPSGD_OK && !blocked && t_enq < end && (int)pend.size() < kRing) {
-            const int64_t to_sync = std::max<int64_t>(p_known - cnt_enq, 1);
-            if (t_enq + to_sync > end) {   // the run ends inside this period
-                if ((status = enqueue_steps(c, t_enq, end - t_enq))) break;
-                cnt_enq += end - t_enq;
-                t_enq = end;
-                break;
+        while (status == ADPSGD_OK && plan.t < end && (int)pend.size() < kRing && (!blocked || lookahead > 0)) {
+            const int64_t t = plan.t;
+            int32_t due = 0;
+            if ((status = adpsgd_sched_step(&hp, &plan, &due))) break;
+            if (blocked) {
+                // cnt <= max(p-1, 1) - 1 < p - 1: no period ends here for any p' >= p - 1
+                --lookahead;
+                if (due) { status = fail(ADPSGD_ESTATE, "internal: sync due inside the look-ahead"); break; }
             }
-            if ((status = enqueue_steps(c, t_enq, to_sync - 1))) break;
-            t_enq += to_sync - 1;
+            if (!due) {
+                status = enqueue_steps(c, t, 1);
+                continue;
+            }
             const int slot = (int)(n_enq_syncs % kRing);
-            if ((status = enqueue_sync(c, true, t_enq, slot))) break;
-            const bool decisive = adaptive && t_enq >= hp.k_s;
-            pend.push_back(Pending{t_enq, p_known, slot, decisive});
+            if ((status = enqueue_sync(c, true, t, slot))) break;
+            const bool decisive = adaptive && t >= hp.k_s && t >= hp.sync_warmup_steps;
+            pend.push_back(Pending{t, plan.p, slot, decisive});
             ++n_enq_syncs;
-            t_enq += 1;
-            cnt_enq = 0;
+            plan.cnt = 0;
             if (decisive) {
-                // p moves by at most one, so the next period has at least
-                // max(p-1, 1) steps; run those while the variance is read back
-                const int64_t pre = std::min<int64_t>(std::max(p_known - 1, 1) - 1, end - t_enq);
-                if ((status = enqueue_steps(c, t_enq, pre))) break;
-                t_enq += pre;
-                cnt_enq = pre;
                 blocked = true;
+                lookahead = std::max(plan.p - 1, 1) - 1;
             }
         }
         if (pend.empty() || status != ADPSGD_OK) break;
@@ -500,18 +499,21 @@ extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, 
         ++n_done;
         if (rc) { status = rc; break; }
         if (q.decisive) {
-            p_known = c->st.p;
+            plan.p = c->st.p;
             blocked = false;
+            lookahead = 0;
         }
         if (c->timing) {
             int hr = harvest(c, false);
             if (hr) { status = hr; break; }
         }
     }
-    // whatever was enqueued runs to completion; the state reflects it
+    // whatever was enqueued runs to completion; the state reflects it (on an
+    // error, p keeps the value in force before the failing sync)
     hipError_t e = hipStreamSynchronize(c->stream);
-    c->st.t = t_enq;
-    c->st.cnt = cnt_enq;
+    c->st.t = plan.t;
+    c->st.cnt = plan.cnt;
+    if (!blocked) c->st.p = plan.p;
     if (n_syncs) *n_syncs = n_done;
     if (status != ADPSGD_OK) return status;
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");

@@ -58,17 +58,47 @@ def test_learning_rate_matches_oracle(A, key):
 
 
 def _lib_trace(A, w, S_fn):
+    """The library's own schedule (sched_step + sched_on_sync) on scripted S."""
     hp = A.hparams_of(w)
     st = A.adpsgd_sched_init(hp)
     out = []
     for t in range(w.total_steps):
-        st.cnt += 1
-        if st.cnt == st.p:
-            st.cnt = 0
-            p_used = st.p
+        if A.adpsgd_sched_step(hp, st):
+            out.append((t, st.p))
             A.adpsgd_sched_on_sync(hp, st, t, S_fn(t, A.adpsgd_lr(hp, t)))
-            out.append((t, p_used))
     return out, st
+
+
+_VARIANTS = {
+    "warmup_adaptive": dict(sync_warmup_steps=250, k_s=600, p_init=4, lr_kind=W.LR_WARMUP_STEP),
+    "alg1_const": dict(period_mode=W.PERIOD_ALG1, p_init=7),
+    "two_phase_up": dict(period_mode=W.PERIOD_CONST, p_init=4, p_switch_step=1500, p_after=8),
+    "two_phase_down": dict(period_mode=W.PERIOD_CONST, p_init=20, p_switch_step=1500, p_after=5),
+    "alg1_two_phase_warmup": dict(period_mode=W.PERIOD_ALG1, p_init=6, p_switch_step=1000, p_after=3,
+                                  sync_warmup_steps=37),
+}
+
+
+@pytest.mark.parametrize("variant", list(_VARIANTS))
+def test_schedule_variants_match_oracle(A, variant):
+    w = W.full_workloads()["resnet18_like"].replace(total_steps=3000, **_VARIANTS[variant])
+    rng = np.random.default_rng(11)
+    noise = rng.lognormal(0.0, 0.35, size=3000)
+    S_fn = lambda t, g: float(noise[t] * g * (0.9 + 0.3 * math.sin(t / 300.0)))
+    lib, st_l = _lib_trace(A, w, S_fn)
+    orc, st_o = oracle.controller_trace(w, S_fn)
+    assert lib == orc
+    assert (st_l.p, st_l.cnt, st_l.nC2) == (st_o.p, st_o.cnt, st_o.nC2)
+    assert st_l.C2 == pytest.approx(st_o.C2, rel=1e-12)
+
+
+def test_warmup_lr_matches_oracle(A):
+    for N in (90, 900, 1000, 50):
+        w = W.full_workloads()["resnet18_like"].replace(total_steps=N, lr_kind=W.LR_WARMUP_STEP)
+        hp = A.hparams_of(w)
+        o = oracle.Oracle(w)
+        for t in range(N):
+            assert A.adpsgd_lr(hp, t) == pytest.approx(o.lr(t), rel=1e-14), (N, t)
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
@@ -139,7 +169,8 @@ def test_constant_mode_never_changes_period(A):
 @pytest.mark.parametrize("field,value", [
     ("sigma", -1.0), ("momentum", 1.0), ("weight_decay", -1e-4), ("h_lo", 0.0), ("h_hi", 1e-9),
     ("lr_kind", 7), ("period_mode", 3), ("lr0", 0.0), ("total_steps", 0), ("p_init", 0),
-    ("k_s", -1), ("thr_lo", 2.0), ("p_max", 2),
+    ("k_s", -1), ("thr_lo", 2.0), ("p_max", 2), ("lr_kind", 4), ("sync_warmup_steps", -1),
+    ("p_switch_step", -1), ("avg_momentum", 2),
 ])
 def test_invalid_hparams_rejected(A, field, value):
     hp, _ = _hp(A)
@@ -147,6 +178,17 @@ def test_invalid_hparams_rejected(A, field, value):
     with pytest.raises(A.AdpsgdError) as e:
         A.adpsgd_sched_init(hp)
     assert e.value.code == A.EINVAL and A.adpsgd_last_error()
+
+
+def test_period_switch_needs_constant_mode_and_valid_period(A):
+    hp, _ = _hp(A)                       # adaptive
+    hp.p_switch_step, hp.p_after = 100, 4
+    with pytest.raises(A.AdpsgdError):
+        A.adpsgd_sched_init(hp)
+    hp, _ = _hp(A, period_mode=W.PERIOD_CONST)
+    hp.p_switch_step, hp.p_after = 100, 0
+    with pytest.raises(A.AdpsgdError):
+        A.adpsgd_sched_init(hp)
 
 
 def _fake_buffers(A, ws=1 << 20, misalign=0):

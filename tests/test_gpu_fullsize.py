@@ -28,6 +28,7 @@ VAR_TOL = 1e-3
 # set by the fp32 rounding of the x it integrates, not by its own size, so m is
 # judged against max(|m|, rms of its tensor) instead of a 1e-2 rms floor.
 MOM_FLOOR = 1.0
+MOM_TOL = 10 * PARAM_TOL     # m integrates gradient errors with gain 1 / (1 - momentum)
 
 
 def _say(msg):
@@ -107,12 +108,12 @@ def test_full_size_run(A, key):
     assert max_rel_err(xs_sel.mean(axis=0), xbar, sub_off) < PARAM_TOL
     # the mean of K momenta cancels most of their noise; its error comes from
     # the replicas, so it is judged on the replicas' rms
-    assert max_rel_err(ms_sel.mean(axis=0), vbar, sub_off, floor=MOM_FLOOR, scale_of=ms_sel) < PARAM_TOL
+    assert max_rel_err(ms_sel.mean(axis=0), vbar, sub_off, floor=MOM_FLOOR, scale_of=ms_sel) < MOM_TOL
 
     if w.period_mode == W.PERIOD_CONST:
         r = o.run(idx=idx)
         assert np.array_equal(recs["t"], r.sync_t)
         assert max_rel_err(xs_sel, r.x, sub_off) < PARAM_TOL
-        assert max_rel_err(ms_sel, r.v, sub_off, floor=MOM_FLOOR) < PARAM_TOL
+        assert max_rel_err(ms_sel, r.v, sub_off, floor=MOM_FLOOR) < MOM_TOL
         for tau in whole:
             assert rel_err(var[:, tau], r.var[:, tau]) < VAR_TOL, tau

@@ -163,8 +163,8 @@ def _adaptive(**kw):
 
 def test_controller_sampling_phase_keeps_p_and_averages():
     w = _adaptive()
-    vals = iter([3.0, 5.0, 10.0, 2.0] + [0.0] * 1000)
-    syncs, st = oracle.controller_trace(w, lambda t, g: next(vals) * g)
+    first = {3: 3.0, 7: 5.0, 11: 10.0, 15: 2.0}          # S / gamma at the first four syncs
+    syncs, st = oracle.controller_trace(w, lambda t, g: first.get(t, 0.0) * g)
     # first 25 syncs (t = 3, 7, ..., 99) are in the sampling phase: p stays 4
     assert [p for t, p in syncs if t < 100] == [4] * 25
     # C2 is the plain mean of S/gamma over the sampling syncs
@@ -391,3 +391,79 @@ def test_sync_variance_matches_closed_form(mu, wd, p):
     mean = samples.mean(axis=0)
     se = samples.std(axis=0, ddof=1) / np.sqrt(R)
     assert np.all(np.abs(mean - want) < 4 * se + 1e-12), (mean, want, se)
+
+
+# ---------------------------------------------------------------- schedule variants
+
+def test_gradual_warmup_learning_rate_matches_paper():
+    for N, t, ratio in _facts("lr_warmup"):
+        w = _tiny(lr_kind=W.LR_WARMUP_STEP, lr0=0.1, total_steps=int(N))
+        assert oracle.lr(w, int(t)) == pytest.approx(0.1 * float(ratio), rel=1e-12), (N, t)
+
+
+def test_algorithm1_sync_offset_matches_paper():
+    for steps, p, want in _facts("alg1"):
+        steps, p = int(steps), int(p)
+        w = _tiny(total_steps=steps, p_init=p, period_mode=W.PERIOD_ALG1)
+        syncs, _ = oracle.controller_trace(w, lambda t, g: 1.0)
+        assert [t for t, _ in syncs] == list(range(0, steps, p))
+        assert len(syncs) == int(want)
+
+
+def test_two_phase_periods_in_one_run_match_paper_counts():
+    for phases, want in _facts("syncs"):
+        ph = [tuple(int(v) for v in x.split(":")) for x in phases.split(",")]
+        if len(ph) != 2:
+            continue
+        (s1, p1), (s2, p2) = ph
+        w = _tiny(total_steps=s1 + s2, p_init=p1, period_mode=W.PERIOD_CONST,
+                  p_switch_step=s1, p_after=p2)
+        syncs, st = oracle.controller_trace(w, lambda t, g: 1.0)
+        assert len(syncs) == int(want)
+        assert {p for t, p in syncs if t < s1} == {p1} and {p for t, p in syncs if t >= s1} == {p2}
+
+
+def test_sync_warmup_prefix_then_algorithm2():
+    # Sections III-B / IV-C: a p = 1 warm-up, then Algorithm 2 from p_init with a
+    # fresh counter; the warm-up syncs do not feed C2.
+    w = _tiny(total_steps=200, period_mode=W.PERIOD_ADAPTIVE, p_init=4, k_s=60, sync_warmup_steps=25)
+    syncs, st = oracle.controller_trace(w, lambda t, g: 2.0 * g)
+    ts = [t for t, _ in syncs]
+    assert ts[:25] == list(range(25)) and {p for t, p in syncs if t < 25} == {4}
+    assert ts[25:30] == [28, 32, 36, 40, 44]
+    assert st.nC2 == len([t for t in ts if 25 <= t < 60]) and st.C2 == pytest.approx(2.0, rel=1e-14)
+
+
+def test_momentum_averaging_makes_period_one_exact_fullsgd():
+    w = _tiny(K=4, sizes=(30,), p_init=1, total_steps=25, weight_decay=5e-4, avg_momentum=True)
+    o = oracle.Oracle(w)
+    r = o.run()
+    for k in range(1, 4):
+        assert np.array_equal(r.x[k], r.x[0]) and np.array_equal(r.v[k], r.v[0])
+    xbar, vbar = o.mean_trajectory(25, h=r.h, xs=r.xs)
+    np.testing.assert_allclose(r.x[0], xbar, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(r.v[0], vbar, rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("mu,p", [(0.9, 3), (0.9, 8)])
+def test_sync_variance_closed_form_with_momentum_averaging(mu, p):
+    # Averaging the momentum as well zeroes the whole deviation state (e, u) at
+    # a sync, so every period restarts from zero covariance.
+    K, P, R, N, wd = 4, 2048, 40, 4 * p, 5e-4
+    w0 = _tiny(K=K, sizes=(P,), momentum=mu, weight_decay=wd, sigma=0.1, lr0=0.1,
+               total_steps=N, p_init=p, avg_momentum=True)
+    h, _ = oracle.problem_data(w0)
+    a = h + wd
+    q = 0.1 * 0.1 * (K - 1) / K
+    Cee = np.zeros_like(h); Ceu = np.zeros_like(h); Cuu = np.zeros_like(h)
+    for t in range(p):
+        uu = mu * mu * Cuu + 2 * mu * a * Ceu + a * a * Cee + q
+        ue = mu * Ceu + a * Cee
+        Cee, Ceu, Cuu = Cee - 2 * 0.1 * ue + 0.01 * uu, ue - 0.1 * uu, uu
+    want = Cee.sum()
+    samples = np.array([oracle.Oracle(w0.replace(seed=2000 + r)).run(h=h).S for r in range(R)])
+    mean, se = samples.mean(axis=0), samples.std(axis=0, ddof=1) / np.sqrt(R)
+    assert np.all(np.abs(mean - want) < 4 * se), (mean, want, se)
+    # and it differs from the local-momentum reading after the first period
+    local = _expected_sync_variance(h, wd, 0.1, mu, 0.1, K, set(range(p - 1, N, p)), N)
+    assert abs(local[-1] - want) > 8 * se.max()

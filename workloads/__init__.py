@@ -25,8 +25,8 @@ from typing import List, Optional
 
 import numpy as np
 
-LR_CONST, LR_STEP, LR_COSINE = 0, 1, 2
-PERIOD_CONST, PERIOD_ADAPTIVE = 0, 1
+LR_CONST, LR_STEP, LR_COSINE, LR_WARMUP_STEP = 0, 1, 2, 3
+PERIOD_CONST, PERIOD_ADAPTIVE, PERIOD_ALG1 = 0, 1, 2
 
 
 @dataclasses.dataclass(frozen=True)
@@ -50,6 +50,10 @@ class Workload:
     k_s: int                  # end of the C2 sampling phase (step index)
     thr_lo: float = 0.7       # Algorithm 2 thresholds
     thr_hi: float = 1.3
+    sync_warmup_steps: int = 0   # steps synced every step before Algorithm 2 starts
+    p_switch_step: int = 0       # constant modes: the period becomes p_after from this step
+    p_after: int = 0
+    avg_momentum: bool = False   # average the momentum buffers at a sync as well
 
     @property
     def P(self) -> int:
