@@ -85,6 +85,8 @@ def main():
     ap.add_argument("--workload", default="vgg16_adaptive")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-timing", action="store_true", help="skip per-kernel HIP events")
+    ap.add_argument("--traced", action="store_true",
+                    help="run the tracing mode (per-step variance and gradient norm) instead")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (x3), to scale byte counters")
     args = ap.parse_args()
@@ -113,6 +115,8 @@ def main():
 
     def one_run():
         eng.reset()
+        if args.traced:
+            return eng.run_traced(N, log_cap=N, with_var=False)[:3]
         return eng.run(N, log_cap=N, with_var=False)
 
     for _ in range(args.warmup):
@@ -150,6 +154,11 @@ def main():
                    "period": "adaptive, p_init 4, K_s 125, thresholds 0.7/1.3",
                    "syncs_per_run": int(n_syncs[-1])},
     }
+    if args.traced:
+        out["config"]["mode"] = "traced"
+    if tm.trace_launches > 0:
+        trace_ms = tm.trace_ms / tm.trace_launches
+        out["traced_step"] = {"avg_launch_ms": trace_ms, "achieved_GBs": step_bytes / (trace_ms * 1e-3) / 1e9}
     if tm.step_launches > 0:
         step_ms = tm.step_ms / tm.step_launches
         achieved = step_bytes / (step_ms * 1e-3) / 1e9

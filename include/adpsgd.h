@@ -134,12 +134,28 @@ typedef struct {
                         S / (thr * gamma * C2) - 1; NaN when no decision made  */
 } adpsgd_sync_rec;
 
+/* One record per local step of a traced run. */
+typedef struct {
+    int64_t t;          /* the step                                                   */
+    int32_t synced;     /* 1 if a sync followed it                                    */
+    int32_t p;          /* period in force                                            */
+    double var;         /* inter-worker parameter variance after step t and before any
+                           sync: sum over tensors of (1/K) sum_k |x_k - xbar|^2, i.e.
+                           Var[W_{t+1}] of Sec. II-B (equal to S at a sync step)      */
+    double grad_norm2;  /* |grad F(xbar)|^2 at the replica mean after step t, with
+                           F(x) = 1/2 sum h (x - x*)^2 + wd/2 |x|^2: the quantity whose
+                           gamma-weighted average is the convergence metric of
+                           eq. (metric1)                                              */
+    double gamma;       /* learning rate of step t                                    */
+} adpsgd_step_rec;
+
 /* Per-kernel device time, from HIP events around each launch when enabled. */
 typedef struct {
     double step_ms;     int64_t step_launches;     /* plain local step            */
     double fused_ms;    int64_t fused_launches;    /* last step of a period + sync */
     double average_ms;  int64_t average_launches;  /* separate mean/broadcast/var */
     double segsum_ms;   int64_t segsum_launches;   /* per-tensor variance sums    */
+    double trace_ms;    int64_t trace_launches;    /* traced plain step (step + variance) */
 } adpsgd_timing;
 
 /* Bytes of device workspace for K workers, P parameters and T tensors with
@@ -190,6 +206,17 @@ ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
  * steps already enqueued after it complete and are counted in the state. */
 ADPSGD_API int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
                double *var_log, int64_t *n_syncs);
+
+/* adpsgd_run that also records every step in trace[0 .. trace_cap) (host):
+ * plain steps run as a step that also reduces the variance and the gradient
+ * norm at the mean without averaging (the same HBM traffic as a plain step),
+ * sync steps as the fused step + sync that also reports the gradient norm.
+ * The period-averaged variance V_t of Sec. III-A (eq. (vt)) follows from the
+ * records: Var[W_k] is 0 at the first step of a period and trace[k-1].var at
+ * the others. */
+ADPSGD_API int adpsgd_run_traced(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
+                                 double *var_log, adpsgd_step_rec *trace, int64_t trace_cap,
+                                 int64_t *n_syncs);
 
 ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
 /* Restore a state saved by adpsgd_get_state (x, m restored by the caller):

@@ -314,6 +314,51 @@ double orc_average(const orc_problem *pb, const int64_t *idx, int64_t n, double 
     return S;
 }
 
+/* The inter-worker variance of the current replicas without averaging them:
+ * var_tau = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2, and their sum
+ * Var[W] of Section II-B (returned). */
+double orc_variance(const orc_problem *pb, const int64_t *idx, int64_t n, const double *x, double *var_out)
+{
+    const int32_t K = pb->K;
+    double *xbar = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    for (int64_t j = 0; j < n; ++j) {
+        double s = 0.0;
+        for (int32_t k = 0; k < K; ++k) s += x[(int64_t)k * n + j];
+        xbar[j] = s / (double)K;
+    }
+    double S = 0.0;
+    for (int32_t tau = 0; tau < pb->T; ++tau) {
+        int64_t jb, je;
+        tensor_range(pb, idx, n, tau, &jb, &je);
+        double acc = 0.0;
+        for (int32_t k = 0; k < K; ++k)
+            for (int64_t j = jb; j < je; ++j) {
+                double dev = xbar[j] - x[(int64_t)k * n + j];
+                acc += dev * dev;
+            }
+        var_out[tau] = acc / (double)K;
+        S += var_out[tau];
+    }
+    free(xbar);
+    return S;
+}
+
+/* |grad F(xbar)|^2 at the replica mean, F(x) = 1/2 sum h (x - x*)^2 + wd/2 |x|^2:
+ * the gradient norm whose gamma-weighted average over iterations is the
+ * convergence metric of eq. (metric1). */
+double orc_grad_norm2(const orc_problem *pb, int64_t n, const double *x, const double *h, const double *xs)
+{
+    double acc = 0.0;
+    for (int64_t j = 0; j < n; ++j) {
+        double s = 0.0;
+        for (int32_t k = 0; k < pb->K; ++k) s += x[(int64_t)k * n + j];
+        double xbar = s / (double)pb->K;
+        double g = h[j] * (xbar - xs[j]) + pb->weight_decay * xbar;
+        acc += g * g;
+    }
+    return acc;
+}
+
 /* Period controller after a sync at step t with variance S (Algorithm 2,
  * lines 13-19).  Inactive in the constant modes and during the warm-up prefix
  * (there the run synchronizes every step and Algorithm 2 has not started).
@@ -381,10 +426,12 @@ int64_t orc_schedule_trace(const orc_problem *pb, orc_state *st, int64_t n_steps
  * period, where the sync schedule does not depend on the data).
  * x, v: [K][n], updated in place.  Each sync appends a record to log (up to
  * log_cap) and its per-tensor variances to var_log[cap][T] (if non-NULL).
- * Returns the number of syncs, or a negative error. */
+ * If trace_var / trace_gn are given ([n_steps] each), every step records the
+ * variance of the replicas after it, before any sync (Var[W_{t+1}]), and
+ * |grad F|^2 at their mean.  Returns the number of syncs, or a negative error. */
 int64_t orc_run(const orc_problem *pb, const int64_t *idx, int64_t n, orc_state *st,
                 int64_t n_steps, const double *h, const double *xs, double *x, double *v,
-                orc_sync_rec *log, int64_t log_cap, double *var_log)
+                orc_sync_rec *log, int64_t log_cap, double *var_log, double *trace_var, double *trace_gn)
 {
     if (idx && n != pb->P && pb->period_mode == 1) return -1;
     double *var = (double *)malloc((size_t)pb->T * sizeof(double));
@@ -393,6 +440,8 @@ int64_t orc_run(const orc_problem *pb, const int64_t *idx, int64_t n, orc_state 
         int64_t t = st->t;
         int sync = begin_step(pb, st, t);
         orc_local_step(pb, idx, n, t, h, xs, x, v);
+        if (trace_var) trace_var[s] = orc_variance(pb, idx, n, x, var);
+        if (trace_gn) trace_gn[s] = orc_grad_norm2(pb, n, x, h, xs);
         if (sync) {
             st->cnt = 0;
             double S = orc_average(pb, idx, n, x, v, var);

@@ -89,7 +89,11 @@ def _load():
         lib.orc_controller.restype = C.c_int
         lib.orc_state_init.argtypes = [C.POINTER(_Problem), C.POINTER(_State)]
         lib.orc_run.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, C.POINTER(_State), C.c_int64,
-                                _D, _D, _D, _D, C.POINTER(_Sync), C.c_int64, _D]
+                                _D, _D, _D, _D, C.POINTER(_Sync), C.c_int64, _D, _D, _D]
+        lib.orc_variance.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, _D, _D]
+        lib.orc_variance.restype = C.c_double
+        lib.orc_grad_norm2.argtypes = [C.POINTER(_Problem), C.c_int64, _D, _D, _D]
+        lib.orc_grad_norm2.restype = C.c_double
         lib.orc_run.restype = C.c_int64
         lib.orc_mean_trajectory.argtypes = [C.POINTER(_Problem), _I64, C.c_int64, C.c_int64,
                                             C.c_int64, _D, _D, _D, _D]
@@ -200,7 +204,10 @@ class Oracle:
         return int(self.lib.orc_controller(C.byref(self.pb), C.byref(st), t, S))
 
     def run(self, n_steps: Optional[int] = None, idx: Optional[np.ndarray] = None,
-            h=None, xs=None, x=None, v=None, state=None, log_cap: Optional[int] = None):
+            h=None, xs=None, x=None, v=None, state=None, log_cap: Optional[int] = None,
+            trace: bool = False):
+        """Algorithm 2 for n_steps steps.  trace=True also records, per step, the
+        replicas' variance before any sync and |grad F|^2 at their mean."""
         w = self.w
         n_steps = w.total_steps if n_steps is None else n_steps
         n = w.P if idx is None else len(idx)
@@ -217,8 +224,10 @@ class Oracle:
         cap = n_steps if log_cap is None else log_cap
         log = (_Sync * max(cap, 1))()
         var_log = np.zeros((max(cap, 1), w.T))
+        tv = np.zeros(max(n_steps, 1)) if trace else None
+        tg = np.zeros(max(n_steps, 1)) if trace else None
         rc = self.lib.orc_run(C.byref(self.pb), _ip(idx), n, C.byref(st), n_steps,
-                              _dp(h), _dp(xs), _dp(x), _dp(v), log, cap, _dp(var_log))
+                              _dp(h), _dp(xs), _dp(x), _dp(v), log, cap, _dp(var_log), _dp(tv), _dp(tg))
         if rc < 0:
             raise RuntimeError(f"oracle run failed: {rc}")
         k = min(int(rc), cap)
@@ -227,7 +236,18 @@ class Oracle:
                          sync_t=np.array([r[0] for r in recs], dtype=np.int64),
                          sync_p=np.array([r[1] for r in recs], dtype=np.int64),
                          S=np.array([r[2] for r in recs]), C2=np.array([r[3] for r in recs]),
-                         gamma=np.array([r[4] for r in recs]), var=var_log[:k].copy())
+                         gamma=np.array([r[4] for r in recs]), var=var_log[:k].copy(),
+                         trace_var=None if tv is None else tv[:n_steps].copy(),
+                         trace_grad_norm2=None if tg is None else tg[:n_steps].copy())
+
+    def variance(self, x, idx=None):
+        """The replicas' variance without averaging them: (Var[W], per-tensor terms)."""
+        var = np.zeros(self.w.T)
+        S = self.lib.orc_variance(C.byref(self.pb), _ip(idx), x.shape[1], _dp(x), _dp(var))
+        return float(S), var
+
+    def grad_norm2(self, x, h, xs):
+        return float(self.lib.orc_grad_norm2(C.byref(self.pb), x.shape[1], _dp(x), _dp(h), _dp(xs)))
 
     def mean_trajectory(self, n_steps, idx=None, h=None, xs=None, t0=0, xbar=None, vbar=None):
         n = self.w.P if idx is None else len(idx)
@@ -256,6 +276,8 @@ class OracleRun:
     C2: np.ndarray
     gamma: np.ndarray
     var: np.ndarray
+    trace_var: Optional[np.ndarray] = None
+    trace_grad_norm2: Optional[np.ndarray] = None
 
 
 def problem_data(w, idx=None):

@@ -15,6 +15,7 @@ from ._native import (  # noqa: F401
     LR_STEP, LR_WARMUP_STEP, OK, PERIOD_ADAPTIVE, PERIOD_ALG1, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
     adpsgd_get_state, adpsgd_get_timing, adpsgd_hparams, adpsgd_init, adpsgd_last_error,
     adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,
+    adpsgd_run_traced, adpsgd_step_rec,
     adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_state, adpsgd_set_timing,
     adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
     make_hparams,
@@ -85,6 +86,9 @@ class Adpsgd:
 
     def run(self, n_steps: int, log_cap: Optional[int] = None, with_var: bool = True):
         return adpsgd_run(self.ctx, n_steps, self.T, log_cap=log_cap, with_var=with_var)
+
+    def run_traced(self, n_steps: int, log_cap: Optional[int] = None, with_var: bool = True):
+        return adpsgd_run_traced(self.ctx, n_steps, self.T, log_cap=log_cap, with_var=with_var)
 
     def reset(self) -> None:
         adpsgd_reset(self.ctx)

@@ -56,11 +56,17 @@ class adpsgd_sync_rec(C.Structure):
                 ("C2", C.c_double), ("gamma", C.c_double), ("margin", C.c_double)]
 
 
+class adpsgd_step_rec(C.Structure):
+    _fields_ = [("t", C.c_int64), ("synced", C.c_int32), ("p", C.c_int32), ("var", C.c_double),
+                ("grad_norm2", C.c_double), ("gamma", C.c_double)]
+
+
 class adpsgd_timing(C.Structure):
     _fields_ = [("step_ms", C.c_double), ("step_launches", C.c_int64),
                 ("fused_ms", C.c_double), ("fused_launches", C.c_int64),
                 ("average_ms", C.c_double), ("average_launches", C.c_int64),
-                ("segsum_ms", C.c_double), ("segsum_launches", C.c_int64)]
+                ("segsum_ms", C.c_double), ("segsum_launches", C.c_int64),
+                ("trace_ms", C.c_double), ("trace_launches", C.c_int64)]
 
 
 if not os.path.exists(LIB_PATH):
@@ -82,6 +88,8 @@ _SIGS = {
     "adpsgd_step_average": (C.c_int, [_CTX, _DP]),
     "adpsgd_schedule": (C.c_int, [_CTX, _DP, C.POINTER(C.c_int32)]),
     "adpsgd_run": (C.c_int, [_CTX, C.c_int64, C.POINTER(adpsgd_sync_rec), C.c_int64, _DP, _I64P]),
+    "adpsgd_run_traced": (C.c_int, [_CTX, C.c_int64, C.POINTER(adpsgd_sync_rec), C.c_int64, _DP,
+                                    C.POINTER(adpsgd_step_rec), C.c_int64, _I64P]),
     "adpsgd_get_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
     "adpsgd_set_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
     "adpsgd_set_timing": (C.c_int, [_CTX, C.c_int32]),
@@ -186,6 +194,32 @@ def adpsgd_run(ctx: int, n_steps: int, T: int, log_cap: Optional[int] = None, wi
         r = log[i]
         recs[i] = (r.t, r.p, r.S, r.C2, r.gamma, r.margin)
     return recs, (None if var_log is None else var_log[:k].copy()), n.value
+
+
+def adpsgd_run_traced(ctx: int, n_steps: int, T: int, log_cap: Optional[int] = None, with_var: bool = True):
+    """adpsgd_run plus one record per step; returns (records, var_log, n_syncs, steps).
+
+    steps is a structured array with fields t, synced, p, var, grad_norm2, gamma."""
+    cap = n_steps if log_cap is None else log_cap
+    log = (adpsgd_sync_rec * max(cap, 1))()
+    var_log = np.zeros((max(cap, 1), T)) if with_var else None
+    trace = (adpsgd_step_rec * max(n_steps, 1))()
+    n = C.c_int64()
+    _check(lib.adpsgd_run_traced(ctx, n_steps, log, cap,
+                                 None if var_log is None else var_log.ctypes.data_as(_DP),
+                                 trace, n_steps, C.byref(n)))
+    k = min(n.value, cap)
+    recs = np.zeros(k, dtype=[("t", np.int64), ("p", np.int32), ("S", np.float64), ("C2", np.float64),
+                              ("gamma", np.float64), ("margin", np.float64)])
+    for i in range(k):
+        r = log[i]
+        recs[i] = (r.t, r.p, r.S, r.C2, r.gamma, r.margin)
+    steps = np.zeros(n_steps, dtype=[("t", np.int64), ("synced", np.int32), ("p", np.int32),
+                                     ("var", np.float64), ("grad_norm2", np.float64), ("gamma", np.float64)])
+    for i in range(n_steps):
+        r = trace[i]
+        steps[i] = (r.t, r.synced, r.p, r.var, r.grad_norm2, r.gamma)
+    return recs, (None if var_log is None else var_log[:k].copy()), n.value, steps
 
 
 def adpsgd_get_state(ctx: int) -> adpsgd_state:

@@ -81,25 +81,47 @@ __device__ __forceinline__ void sgd_update(const StepParams &a, f4 &x, f4 &m, f4
     x = fma4(splat(-a.gamma), m, x);
 }
 
-// Sum over the block in a fixed order: wave64 butterfly, then the waves in
-// order.  Valid on thread 0.
+// Sums of a pair of values over the block in a fixed order: wave64 butterfly,
+// then the waves in order.  Valid on thread 0.
+struct Pair {
+    double a, b;
+};
 template <int WAVES>
-__device__ __forceinline__ double block_sum(double v) {
+__device__ __forceinline__ Pair block_sum2(double a, double b) {
 #pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    for (int off = 32; off >= 1; off >>= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+    }
     if constexpr (WAVES == 1) {
-        return v;
+        return Pair{a, b};
     } else {
-        __shared__ double wave_sum[WAVES];
-        if ((threadIdx.x & 63) == 0) wave_sum[threadIdx.x >> 6] = v;
+        __shared__ double wave_a[WAVES], wave_b[WAVES];
+        if ((threadIdx.x & 63) == 0) {
+            wave_a[threadIdx.x >> 6] = a;
+            wave_b[threadIdx.x >> 6] = b;
+        }
         __syncthreads();
-        double total = 0.0;
+        Pair total{0.0, 0.0};
         if (threadIdx.x == 0) {
 #pragma unroll
-            for (int w = 0; w < WAVES; ++w) total += wave_sum[w];
+            for (int w = 0; w < WAVES; ++w) {
+                total.a += wave_a[w];
+                total.b += wave_b[w];
+            }
         }
         return total;
     }
+}
+
+// Squared norm of the gradient of F(x) = 1/2 sum h (x - x*)^2 + wd/2 |x|^2 at
+// the replica mean, summed over the lanes of one group in [lo, hi).
+__device__ __forceinline__ double grad_norm2(const StepParams &a, f4 mean, f4 h, f4 xs, bool full, int64_t e0,
+                                             int64_t lo, int64_t hi) {
+    const f4 gr = fma4(h, mean - xs, splat(a.wd) * mean);
+    f4 g2 = gr * gr;
+    if (!full) g2 = mask4(g2, e0, lo, hi);
+    return ((double)g2.x + (double)g2.y) + ((double)g2.z + (double)g2.w);
 }
 
 // ---------------------------------------------------------------- local step
@@ -155,15 +177,21 @@ __device__ __forceinline__ f4 tree_sum_lds(const f4 (*rows)[64], int lane, int b
 
 // One tile (at most 64 groups, one per lane) of one tensor.  Wave w owns the
 // rows k = w, w + W, ... (W = min(K, 16) waves, R = K / W rows each).  Each
-// thread steps its rows (if fused), publishes them in LDS, reads all K rows of
-// its lane back to form the mean in a fixed order (the same bits in every
-// thread), then writes the mean over its rows and sums its squared deviations.
-// AVGM also replaces the momentum rows by their mean, the same way.  Lanes of
-// groups cut by the tile bounds use masked scalar accesses.
-template <int KT, bool VEC, bool NT, bool FUSED, bool AVGM>
+// thread steps its rows (modes with a step), publishes them in LDS, reads all
+// K rows of its lane back to form the mean in a fixed order (the same bits in
+// every thread), sums its squared deviations and, when averaging, writes the
+// mean over its rows (AVGM: the momentum rows too).  Tracing modes also sum
+// the squared gradient norm at the mean (wave 0 counts each element once).
+// partials[2 tile + {0, 1}] = (sum of squared deviations, gradient norm^2).
+// Lanes of groups cut by the tile bounds use masked scalar accesses.
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
 __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParams p) {
     constexpr int W = KT < 16 ? KT : 16;
     constexpr int R = KT / W;
+    constexpr bool STEP = MODE != kAverage;
+    constexpr bool BCAST = MODE != kTrace;
+    constexpr bool GN = MODE == kTrace || MODE == kFusedTrace;
+    static_assert(!AVGM || BCAST, "momentum is averaged only by a sync");
     __shared__ f4 rows[KT][64];
     __shared__ f4 mrows[AVGM ? KT : 1][64];
     const StepParams &a = p.s;
@@ -175,21 +203,23 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
     const bool active = e0 < hi;
     const bool full = VEC && e0 >= lo && e0 + 4 <= hi;
     f4 xr[R];
+    f4 h = splat(0.0f), xs = splat(0.0f);
     if (active) {
-        f4 h = splat(0.0f), xs = splat(0.0f);
         f4 m[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
             xr[r] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
-            if (FUSED || AVGM) {
+            if (STEP || AVGM) {
                 float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
                 m[r] = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
             }
         }
-        if (FUSED) {
+        if (STEP || GN) {
             if (full) { h = ld4<false>(a.h + e0); xs = ld4<false>(a.xs + e0); }
             else { h = ld4_masked(a.h + e0, e0, lo, hi); xs = ld4_masked(a.xs + e0, e0, lo, hi); }
+        }
+        if (STEP) {
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 const int k = w + W * r;
@@ -197,6 +227,10 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
                 if (!AVGM) {
                     float *mrow = a.m + (int64_t)k * a.P + e0;
                     if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
+                }
+                if (!BCAST) {     // tracing: the replicas keep their new values
+                    float *xrow = a.x + (int64_t)k * a.P + e0;
+                    if (full) st4<NT>(xrow, xr[r]); else st4_masked(xrow, xr[r], e0, lo, hi);
                 }
             }
         }
@@ -207,7 +241,7 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
         }
     }
     __syncthreads();
-    double acc = 0.0;
+    double acc = 0.0, gn = 0.0;
     if (active) {
         const f4 mean = tree_sum_lds<KT>(rows, lane, 0) / splat((float)KT);
         f4 dev2 = splat(0.0f);
@@ -215,8 +249,10 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
         for (int r = 0; r < R; ++r) {
             const f4 dk = mean - xr[r];
             dev2 = fma4(dk, dk, dev2);
-            float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
-            if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
+            if (BCAST) {
+                float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
+                if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
+            }
         }
         if (AVGM) {
             const f4 mmean = tree_sum_lds<KT>(mrows, lane, 0) / splat((float)KT);
@@ -228,27 +264,36 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
         }
         if (!full) dev2 = mask4(dev2, e0, lo, hi);
         acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
+        if (GN && w == 0) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
-    const double total = block_sum<W>(acc);
-    if (threadIdx.x == 0) p.partials[blockIdx.x] = total;
+    const Pair total = block_sum2<W>(acc, gn);
+    if (threadIdx.x == 0) {
+        p.partials[2 * (int64_t)blockIdx.x] = total.a;
+        p.partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+    }
 }
 
 // Any K: one wave per tile, lane = group, the workers walked in a loop.  The
-// first pass sums the replicas (stepping and storing them if fused), the
-// second re-reads them for the deviations and writes the mean.  AVGM sums the
-// momentum buffers in the first pass and writes their mean in the second.
-template <bool VEC, bool FUSED, bool AVGM>
+// first pass sums the replicas (stepping and storing them in modes with a
+// step), the second re-reads them for the deviations and, when averaging,
+// writes the mean.  AVGM sums the momentum buffers in the first pass and
+// writes their mean in the second.
+template <bool VEC, int MODE, bool AVGM>
 __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
+    constexpr bool STEP = MODE != kAverage;
+    constexpr bool BCAST = MODE != kTrace;
+    constexpr bool GN = MODE == kTrace || MODE == kFusedTrace;
+    static_assert(!AVGM || BCAST, "momentum is averaged only by a sync");
     const StepParams &a = p.s;
     const Tile tile = p.tiles[blockIdx.x];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
     const int64_t g = (lo >> 2) + threadIdx.x;
     const int64_t e0 = 4 * g;
-    double acc = 0.0;
+    double acc = 0.0, gn = 0.0;
     if (e0 < hi) {
         const bool full = VEC && e0 >= lo && e0 + 4 <= hi;
         f4 h = splat(0.0f), xs = splat(0.0f);
-        if (FUSED) {
+        if (STEP || GN) {
             if (full) { h = ld4<false>(a.h + e0); xs = ld4<false>(a.xs + e0); }
             else { h = ld4_masked(a.h + e0, e0, lo, hi); xs = ld4_masked(a.xs + e0, e0, lo, hi); }
         }
@@ -258,8 +303,8 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             float *mrow = a.m + (int64_t)k * a.P + e0;
             f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
             f4 m = splat(0.0f);
-            if (FUSED || AVGM) m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
-            if (FUSED) {
+            if (STEP || AVGM) m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
+            if (STEP) {
                 sgd_update(a, x, m, h, xs, step_noise(a, g, k));
                 if (full) st4<false>(xrow, x); else st4_masked(xrow, x, e0, lo, hi);
                 if (!AVGM) { if (full) st4<false>(mrow, m); else st4_masked(mrow, m, e0, lo, hi); }
@@ -275,7 +320,7 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
             const f4 dk = mean - x;
             dev2 = fma4(dk, dk, dev2);
-            if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
+            if (BCAST) { if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi); }
             if (AVGM) {
                 float *mrow = a.m + (int64_t)k * a.P + e0;
                 if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
@@ -283,31 +328,49 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
         }
         if (!full) dev2 = mask4(dev2, e0, lo, hi);
         acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
+        if (GN) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
-    const double total = block_sum<1>(acc);
-    if (threadIdx.x == 0) p.partials[blockIdx.x] = total;
+    const Pair total = block_sum2<1>(acc, gn);
+    if (threadIdx.x == 0) {
+        p.partials[2 * (int64_t)blockIdx.x] = total.a;
+        p.partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+    }
 }
 
-// Level 1: the tiles of chunk c are [chunks[c].first, + count), all in one tensor.
+// Level 1: the tiles of chunk c are [chunks[c].first, + count), all in one
+// tensor; both components of their partials are summed.
 __global__ void __launch_bounds__(kBlock) k_seg_chunks(const Chunk *chunks, const double *tile_partials,
                                                       double *chunk_partials) {
     const Chunk c = chunks[blockIdx.x];
-    double acc = 0.0;
-    for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) acc += tile_partials[c.first + i];
-    const double total = block_sum<kBlock / 64>(acc);
-    if (threadIdx.x == 0) chunk_partials[blockIdx.x] = total;
+    double a = 0.0, b = 0.0;
+    for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) {
+        a += tile_partials[2 * (int64_t)(c.first + i)];
+        b += tile_partials[2 * (int64_t)(c.first + i) + 1];
+    }
+    const Pair total = block_sum2<kBlock / 64>(a, b);
+    if (threadIdx.x == 0) {
+        chunk_partials[2 * (int64_t)blockIdx.x] = total.a;
+        chunk_partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+    }
 }
 
-// Level 2: var[tau] = (sum of the partials of tau's chunks) / K; tau's chunks
-// are [chunk_begin[tau], chunk_begin[tau+1]).
+// Level 2, over tau's chunks [chunk_begin[tau], chunk_begin[tau+1]):
+// out[tau] = (sum of squared deviations) / K (the tensor's variance) and
+// out[T + tau] = its gradient norm^2.
 __global__ void __launch_bounds__(kBlock) k_seg_tensors(const int32_t *chunk_begin, const double *chunk_partials,
-                                                       double *var, int32_t K) {
+                                                       double *out, int32_t T, int32_t K) {
     const int32_t tau = blockIdx.x;
     const int32_t b = chunk_begin[tau], e = chunk_begin[tau + 1];
-    double acc = 0.0;
-    for (int32_t i = b + (int32_t)threadIdx.x; i < e; i += kBlock) acc += chunk_partials[i];
-    const double total = block_sum<kBlock / 64>(acc);
-    if (threadIdx.x == 0) var[tau] = total / (double)K;
+    double sa = 0.0, sb = 0.0;
+    for (int32_t i = b + (int32_t)threadIdx.x; i < e; i += kBlock) {
+        sa += chunk_partials[2 * (int64_t)i];
+        sb += chunk_partials[2 * (int64_t)i + 1];
+    }
+    const Pair total = block_sum2<kBlock / 64>(sa, sb);
+    if (threadIdx.x == 0) {
+        out[tau] = total.a / (double)K;
+        out[T + tau] = total.b;
+    }
 }
 
 // ---------------------------------------------------------------- problem data
@@ -343,31 +406,48 @@ __global__ void __launch_bounds__(kBlock) k_normal_dump(RoundKeys rk, uint32_t c
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
 
-template <int KT, bool FUSED, bool AVGM>
+template <int KT, int MODE, bool AVGM>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, hipStream_t st) {
     constexpr int threads = 64 * (KT < 16 ? KT : 16);
     const dim3 grid((unsigned)n_tiles), block(threads);
-    if (vec && nt) k_sync_lds<KT, true, true, FUSED, AVGM><<<grid, block, 0, st>>>(p);
-    else if (vec) k_sync_lds<KT, true, false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
-    else k_sync_lds<KT, false, false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    if (vec && nt) k_sync_lds<KT, true, true, MODE, AVGM><<<grid, block, 0, st>>>(p);
+    else if (vec) k_sync_lds<KT, true, false, MODE, AVGM><<<grid, block, 0, st>>>(p);
+    else k_sync_lds<KT, false, false, MODE, AVGM><<<grid, block, 0, st>>>(p);
     return hipGetLastError();
 }
 
 template <int KT>
-hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec, bool nt,
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,
                          hipStream_t st) {
-    if (fused && avg_m) return sync_dispatch<KT, true, true>(p, n_tiles, vec, nt, st);
-    if (fused) return sync_dispatch<KT, true, false>(p, n_tiles, vec, nt, st);
-    if (avg_m) return sync_dispatch<KT, false, true>(p, n_tiles, vec, nt, st);
-    return sync_dispatch<KT, false, false>(p, n_tiles, vec, nt, st);
+    switch (mode) {
+    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true>(p, n_tiles, vec, nt, st)
+                                : sync_dispatch<KT, kAverage, false>(p, n_tiles, vec, nt, st);
+    case kFused: return avg_m ? sync_dispatch<KT, kFused, true>(p, n_tiles, vec, nt, st)
+                              : sync_dispatch<KT, kFused, false>(p, n_tiles, vec, nt, st);
+    case kTrace: return sync_dispatch<KT, kTrace, false>(p, n_tiles, vec, nt, st);
+    default: return avg_m ? sync_dispatch<KT, kFusedTrace, true>(p, n_tiles, vec, nt, st)
+                          : sync_dispatch<KT, kFusedTrace, false>(p, n_tiles, vec, nt, st);
+    }
 }
 
-template <bool FUSED, bool AVGM>
+template <int MODE, bool AVGM>
 hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, hipStream_t st) {
     const dim3 grid((unsigned)n_tiles), block(64);
-    if (vec) k_sync_loop<true, FUSED, AVGM><<<grid, block, 0, st>>>(p);
-    else k_sync_loop<false, FUSED, AVGM><<<grid, block, 0, st>>>(p);
+    if (vec) k_sync_loop<true, MODE, AVGM><<<grid, block, 0, st>>>(p);
+    else k_sync_loop<false, MODE, AVGM><<<grid, block, 0, st>>>(p);
     return hipGetLastError();
+}
+
+hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, hipStream_t st) {
+    switch (mode) {
+    case kAverage: return avg_m ? loop_dispatch<kAverage, true>(p, n_tiles, vec, st)
+                                : loop_dispatch<kAverage, false>(p, n_tiles, vec, st);
+    case kFused: return avg_m ? loop_dispatch<kFused, true>(p, n_tiles, vec, st)
+                              : loop_dispatch<kFused, false>(p, n_tiles, vec, st);
+    case kTrace: return loop_dispatch<kTrace, false>(p, n_tiles, vec, st);
+    default: return avg_m ? loop_dispatch<kFusedTrace, true>(p, n_tiles, vec, st)
+                          : loop_dispatch<kFusedTrace, false>(p, n_tiles, vec, st);
+    }
 }
 
 }  // namespace
@@ -386,26 +466,23 @@ hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t
     return hipGetLastError();
 }
 
-hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec, bool nt,
+hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,
                             hipStream_t st) {
     if (n_tiles <= 0) return hipSuccess;
+    if (mode == kTrace) avg_m = false;    // nothing is averaged without a sync
     switch (p.s.K) {
-    case 1: return sync_dispatch<1>(p, n_tiles, fused, avg_m, vec, nt, st);
-    case 2: return sync_dispatch<2>(p, n_tiles, fused, avg_m, vec, nt, st);
-    case 4: return sync_dispatch<4>(p, n_tiles, fused, avg_m, vec, nt, st);
-    case 8: return sync_dispatch<8>(p, n_tiles, fused, avg_m, vec, nt, st);
-    case 16: return sync_dispatch<16>(p, n_tiles, fused, avg_m, vec, nt, st);
-    case 32: return sync_dispatch<32>(p, n_tiles, fused, avg_m, vec, nt, st);
-    default:
-        if (fused && avg_m) return loop_dispatch<true, true>(p, n_tiles, vec, st);
-        if (fused) return loop_dispatch<true, false>(p, n_tiles, vec, st);
-        if (avg_m) return loop_dispatch<false, true>(p, n_tiles, vec, st);
-        return loop_dispatch<false, false>(p, n_tiles, vec, st);
+    case 1: return sync_dispatch<1>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 2: return sync_dispatch<2>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 4: return sync_dispatch<4>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 8: return sync_dispatch<8>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 16: return sync_dispatch<16>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 32: return sync_dispatch<32>(p, n_tiles, mode, avg_m, vec, nt, st);
+    default: return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
     }
 }
 
 hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
-                         const double *tile_partials, double *chunk_partials, double *var, int32_t T, int32_t K,
+                         const double *tile_partials, double *chunk_partials, double *out, int32_t T, int32_t K,
                          hipStream_t st) {
     if (n_chunks > 0) {
         k_seg_chunks<<<dim3((unsigned)n_chunks), dim3(kBlock), 0, st>>>(chunks, tile_partials, chunk_partials);
@@ -413,7 +490,7 @@ hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *c
         if (e != hipSuccess) return e;
     }
     if (T <= 0) return hipSuccess;
-    k_seg_tensors<<<dim3((unsigned)T), dim3(kBlock), 0, st>>>(chunk_begin, chunk_partials, var, K);
+    k_seg_tensors<<<dim3((unsigned)T), dim3(kBlock), 0, st>>>(chunk_begin, chunk_partials, out, T, K);
     return hipGetLastError();
 }
 

@@ -42,22 +42,29 @@ struct StepParams {
 struct SyncParams {
     StepParams s;      // x, m, P, K; the step fields are used only when fused
     const Tile *tiles;
-    double *partials;  // [n_tiles] sum over the tile of sum_k (xbar - x_k)^2
+    double *partials;  // [2 n_tiles]: per tile, sum of sum_k (xbar - x_k)^2, gradient norm^2
 };
 
 // Grid size of the local step for n_groups groups and K workers.
 int64_t local_step_blocks(int64_t n_groups, int32_t K);
 // vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4.
 hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, hipStream_t st);
-// fused = true: the local step and the sync in one pass.  avg_m = true: the
-// momentum buffers are averaged as well.
-hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, bool fused, bool avg_m, bool vec,
+// What a sync-tile kernel does: average only (a separate sync), one local step
+// then average (a period's last step), one local step and only measure
+// (tracing: variance and gradient norm at the mean, replicas kept), or one
+// local step, measure and average (a traced period's last step).
+enum SyncMode : int { kAverage = 0, kFused = 1, kTrace = 2, kFusedTrace = 3 };
+
+// Tile partials are pairs (sum of squared deviations, squared gradient norm at
+// the mean; the latter only in the tracing modes).  avg_m = true: a sync also
+// averages the momentum buffers.
+hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec,
                             bool nontemporal, hipStream_t st);
-// chunk_partials[c] = sum of the tile partials of chunk c; then
-// var[tau] = (sum of the partials of tau's chunks) / K, where tau's chunks are
-// [chunk_begin[tau], chunk_begin[tau+1]).
+// chunk_partials[c] = sums of the tile partials of chunk c; then, over tau's
+// chunks [chunk_begin[tau], chunk_begin[tau+1]): out[tau] = variance
+// (deviation sum / K) and out[T + tau] = squared gradient norm.
 hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
-                         const double *tile_partials, double *chunk_partials, double *var, int32_t T,
+                         const double *tile_partials, double *chunk_partials, double *out, int32_t T,
                          int32_t K, hipStream_t st);
 hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, double h_lo,
                                double h_hi, hipStream_t st);

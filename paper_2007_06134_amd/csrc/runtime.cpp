@@ -36,7 +36,7 @@ constexpr int kTimedMax = 1024;    // pending timed launches before a harvest
 constexpr int64_t kMaxK = 65536;
 constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
 
-enum TimedKind { kStep = 0, kFused = 1, kAverage = 2, kSegsum = 3 };
+enum TimedKind { tStep = 0, tFused = 1, tAverage = 2, tSegsum = 3, tTrace = 4, tKinds = 5 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -104,9 +104,9 @@ Layout layout_for(const Plan &pl, int32_t T) {
     l.chunks = align_up(l.tiles + sizeof(Tile) * at_least_one(pl.n_tiles), 256);
     l.chunk_begin = align_up(l.chunks + sizeof(Chunk) * at_least_one(pl.n_chunks), 256);
     l.tile_partials = align_up(l.chunk_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
-    l.chunk_partials = align_up(l.tile_partials + sizeof(double) * at_least_one(pl.n_tiles), 256);
-    l.var = align_up(l.chunk_partials + sizeof(double) * at_least_one(pl.n_chunks), 256);
-    l.total = align_up(l.var + sizeof(double) * (size_t)kRing * (size_t)T, 256);
+    l.chunk_partials = align_up(l.tile_partials + 2 * sizeof(double) * at_least_one(pl.n_tiles), 256);
+    l.var = align_up(l.chunk_partials + 2 * sizeof(double) * at_least_one(pl.n_chunks), 256);
+    l.total = align_up(l.var + sizeof(double) * (size_t)kRing * 2 * (size_t)T, 256);
     return l;
 }
 
@@ -149,8 +149,8 @@ struct adpsgd_ctx {
     int32_t *d_chunk_begin = nullptr;
     double *d_tile_partials = nullptr;
     double *d_chunk_partials = nullptr;
-    double *d_var = nullptr;        // [kRing][T] device
-    double *h_var = nullptr;        // [kRing][T] pinned host
+    double *d_var = nullptr;        // [kRing][2T] device: variances, then gradient norms
+    double *h_var = nullptr;        // [kRing][2T] pinned host
     hipEvent_t ring_ev[kRing] = {};
     adpsgd_state st{};
     bool vec = true;                // P % 4 == 0: dwordx4 rows
@@ -159,8 +159,8 @@ struct adpsgd_ctx {
     bool timing = false;
     std::deque<TimedLaunch> timed;
     std::vector<hipEvent_t> ev_pool;
-    double t_ms[4] = {0, 0, 0, 0};
-    int64_t t_n[4] = {0, 0, 0, 0};
+    double t_ms[tKinds] = {};
+    int64_t t_n[tKinds] = {};
 };
 
 namespace {
@@ -257,31 +257,34 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
 int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
     for (int64_t j = 0; j < n; ++j) {
         const StepParams p = step_params(c, t0 + j);
-        int rc = timed_launch(c, kStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->stream); });
+        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->stream); });
         if (rc) return rc;
     }
     return ok();
 }
 
-// Sync (fused behind step t if fused) with its variances landing in ring slot.
-int enqueue_sync(adpsgd_ctx *c, bool fused, int64_t t, int slot) {
+// A sync-tile kernel of the given mode at step t (the step is used by the
+// modes with a step), with its per-tensor variances (and gradient norms)
+// landing in ring slot `slot`.
+int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot) {
     SyncParams sp;
     sp.s = step_params(c, t);
     sp.tiles = c->d_tiles;
     sp.partials = c->d_tile_partials;
     const int64_t n_tiles = (int64_t)c->tiles.size();
-    int rc = timed_launch(c, fused ? kFused : kAverage, [&] {
-        return launch_tile_sync(sp, n_tiles, fused, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream);
+    const int kind = mode == kAverage ? tAverage : mode == kTrace ? tTrace : tFused;
+    int rc = timed_launch(c, kind, [&] {
+        return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream);
     });
     if (rc) return rc;
-    double *dv = c->d_var + (size_t)slot * c->T;
-    rc = timed_launch(c, kSegsum, [&] {
+    double *dv = c->d_var + (size_t)slot * 2 * c->T;
+    rc = timed_launch(c, tSegsum, [&] {
         return launch_segsum(c->d_chunks, (int64_t)c->chunks.size(), c->d_chunk_begin, c->d_tile_partials,
                              c->d_chunk_partials, dv, c->T, c->K, c->stream);
     });
     if (rc) return rc;
-    HIP_TRY(hipMemcpyAsync(c->h_var + (size_t)slot * c->T, dv, sizeof(double) * c->T, hipMemcpyDeviceToHost,
-                           c->stream));
+    HIP_TRY(hipMemcpyAsync(c->h_var + (size_t)slot * 2 * c->T, dv, 2 * sizeof(double) * c->T,
+                           hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipEventRecord(c->ring_ev[slot], c->stream));
     return ok();
 }
@@ -358,7 +361,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     };
     hipError_t e;
     if ((e = hipGetDevice(&c->device)) != hipSuccess) return bail(e, "hipGetDevice");
-    if ((e = hipHostMalloc((void **)&c->h_var, sizeof(double) * kRing * (size_t)T, hipHostMallocDefault)) != hipSuccess)
+    if ((e = hipHostMalloc((void **)&c->h_var, sizeof(double) * kRing * 2 * (size_t)T, hipHostMallocDefault)) !=
+        hipSuccess)
         return bail(e, "hipHostMalloc");
     for (auto &ev : c->ring_ev)
         if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail(e, "hipEventCreate");
@@ -373,7 +377,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if ((e = hipMemcpyAsync(c->d_chunk_begin, c->chunk_begin.data(), sizeof(int32_t) * (T + 1),
                             hipMemcpyHostToDevice, c->stream)) != hipSuccess)
         return bail(e, "copy chunk offsets");
-    if ((e = hipMemsetAsync(c->d_var, 0, sizeof(double) * kRing * (size_t)T, c->stream)) != hipSuccess)
+    if ((e = hipMemsetAsync(c->d_var, 0, sizeof(double) * kRing * 2 * (size_t)T, c->stream)) != hipSuccess)
         return bail(e, "clear variance ring");
     if (P > 0) {
         if ((e = launch_init_problem(buf->h, buf->xstar, P, hp->seed, hp->h_lo, hp->h_hi, c->stream)) != hipSuccess)
@@ -415,7 +419,7 @@ static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
     if (int rc = check_ctx(c)) return rc;
     if (!var_out) return fail(ADPSGD_EINVAL, "var_out is NULL");
     if (fused && c->st.t + 1 > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
-    if (int rc = enqueue_sync(c, fused, c->st.t, 0)) return rc;
+    if (int rc = enqueue_sync(c, fused ? kFused : kAverage, c->st.t, 0)) return rc;
     HIP_TRY(hipEventSynchronize(c->ring_ev[0]));
     std::memcpy(var_out, c->h_var, sizeof(double) * c->T);
     if (fused) c->st.t += 1;
@@ -436,25 +440,30 @@ extern "C" int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
     return rc;
 }
 
-extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
-                          int64_t *n_syncs) {
+// Algorithm 2 for n_steps steps (adpsgd_run, adpsgd_run_traced).  With a
+// trace, every step takes a ring slot: plain steps run the tracing mode of the
+// sync-tile kernel, sync steps its traced fused mode.
+static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
+                    adpsgd_step_rec *trace, int64_t trace_cap, int64_t *n_syncs) {
     if (int rc = check_ctx(c)) return rc;
-    if (n_steps < 0 || log_cap < 0) return fail(ADPSGD_EINVAL, "n_steps and log_cap must be >= 0");
+    if (n_steps < 0 || log_cap < 0 || trace_cap < 0) return fail(ADPSGD_EINVAL, "n_steps and capacities must be >= 0");
     if (log_cap > 0 && !log) return fail(ADPSGD_EINVAL, "log is NULL with log_cap > 0");
+    if (trace_cap > 0 && !trace) return fail(ADPSGD_EINVAL, "trace is NULL with trace_cap > 0");
     if (c->st.t + n_steps > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
 
     const adpsgd_hparams &hp = c->hp;
     const bool adaptive = hp.period_mode == ADPSGD_PERIOD_ADAPTIVE;
-    const int64_t end = c->st.t + n_steps;
+    const bool traced = trace != nullptr;
+    const int64_t t0 = c->st.t, end = c->st.t + n_steps;
     // plan: the schedule as enqueued on the stream (t, cnt, p).  c->st: the
     // controller's view (p, C2, nC2), advanced as syncs are read back in order.
     // They differ only while a decisive sync (one whose decision may move p) is
     // in flight; then only steps that end no period under p - 1, p or p + 1
     // are enqueued, so the GPU keeps working while the host waits.
     adpsgd_state plan = c->st;
-    struct Pending { int64_t t; int32_t p; int slot; bool decisive; };
+    struct Pending { int64_t t; int32_t p; int slot; bool sync, decisive; };
     std::deque<Pending> pend;
-    int64_t n_enq_syncs = 0, n_done = 0, lookahead = 0;
+    int64_t n_slots = 0, n_done = 0, lookahead = 0;
     bool blocked = false;
     int status = ADPSGD_OK;
 
@@ -468,15 +477,17 @@ extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, 
                 --lookahead;
                 if (due) { status = fail(ADPSGD_ESTATE, "internal: sync due inside the look-ahead"); break; }
             }
-            if (!due) {
+            if (!due && !traced) {
                 status = enqueue_steps(c, t, 1);
                 continue;
             }
-            const int slot = (int)(n_enq_syncs % kRing);
-            if ((status = enqueue_sync(c, true, t, slot))) break;
-            const bool decisive = adaptive && t >= hp.k_s && t >= hp.sync_warmup_steps;
-            pend.push_back(Pending{t, plan.p, slot, decisive});
-            ++n_enq_syncs;
+            const int slot = (int)(n_slots % kRing);
+            const int mode = due ? (traced ? kFusedTrace : kFused) : kTrace;
+            if ((status = enqueue_sync(c, mode, t, slot))) break;
+            ++n_slots;
+            const bool decisive = due && adaptive && t >= hp.k_s && t >= hp.sync_warmup_steps;
+            pend.push_back(Pending{t, plan.p, slot, due != 0, decisive});
+            if (!due) continue;
             plan.cnt = 0;
             if (decisive) {
                 blocked = true;
@@ -488,20 +499,25 @@ extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, 
         pend.pop_front();
         hipError_t e = hipEventSynchronize(c->ring_ev[q.slot]);
         if (e != hipSuccess) { status = hip_fail(e, "wait for variance"); break; }
-        const double *var = c->h_var + (size_t)q.slot * c->T;
+        const double *var = c->h_var + (size_t)q.slot * 2 * c->T;
         const double S = sum_var(var, c->T);
-        double margin = std::numeric_limits<double>::quiet_NaN();
-        const int rc = adpsgd_sched_on_sync(&hp, &c->st, q.t, S, &margin);
-        if (n_done < log_cap) {
-            log[n_done] = adpsgd_sync_rec{q.t, q.p, 0, S, c->st.C2, adpsgd_lr(&hp, q.t), margin};
-            if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
-        }
-        ++n_done;
-        if (rc) { status = rc; break; }
-        if (q.decisive) {
-            plan.p = c->st.p;
-            blocked = false;
-            lookahead = 0;
+        if (traced && q.t - t0 < trace_cap)
+            trace[q.t - t0] = adpsgd_step_rec{q.t, q.sync ? 1 : 0, q.p, S, sum_var(var + c->T, c->T),
+                                              adpsgd_lr(&hp, q.t)};
+        if (q.sync) {
+            double margin = std::numeric_limits<double>::quiet_NaN();
+            const int rc = adpsgd_sched_on_sync(&hp, &c->st, q.t, S, &margin);
+            if (n_done < log_cap) {
+                log[n_done] = adpsgd_sync_rec{q.t, q.p, 0, S, c->st.C2, adpsgd_lr(&hp, q.t), margin};
+                if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
+            }
+            ++n_done;
+            if (rc) { status = rc; break; }
+            if (q.decisive) {
+                plan.p = c->st.p;
+                blocked = false;
+                lookahead = 0;
+            }
         }
         if (c->timing) {
             int hr = harvest(c, false);
@@ -518,6 +534,17 @@ extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, 
     if (status != ADPSGD_OK) return status;
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     return ok();
+}
+
+extern "C" int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
+                          int64_t *n_syncs) {
+    return run_impl(c, n_steps, log, log_cap, var_log, nullptr, 0, n_syncs);
+}
+
+extern "C" int adpsgd_run_traced(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
+                                 double *var_log, adpsgd_step_rec *trace, int64_t trace_cap, int64_t *n_syncs) {
+    if (!trace) return fail(ADPSGD_EINVAL, "trace is NULL");
+    return run_impl(c, n_steps, log, log_cap, var_log, trace, trace_cap, n_syncs);
 }
 
 extern "C" int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out) {
@@ -542,7 +569,7 @@ extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t on) {
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (int rc = harvest(c, true)) return rc;
     c->timing = on != 0;
-    for (int i = 0; i < 4; ++i) { c->t_ms[i] = 0.0; c->t_n[i] = 0; }
+    for (int i = 0; i < tKinds; ++i) { c->t_ms[i] = 0.0; c->t_n[i] = 0; }
     return ok();
 }
 
@@ -551,8 +578,9 @@ extern "C" int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out) {
     if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (int rc = harvest(c, true)) return rc;
-    *out = adpsgd_timing{c->t_ms[kStep], c->t_n[kStep], c->t_ms[kFused], c->t_n[kFused],
-                         c->t_ms[kAverage], c->t_n[kAverage], c->t_ms[kSegsum], c->t_n[kSegsum]};
+    *out = adpsgd_timing{c->t_ms[tStep],  c->t_n[tStep],   c->t_ms[tFused],  c->t_n[tFused],
+                         c->t_ms[tAverage], c->t_n[tAverage], c->t_ms[tSegsum], c->t_n[tSegsum],
+                         c->t_ms[tTrace], c->t_n[tTrace]};
     return ok();
 }
 

@@ -117,3 +117,48 @@ def test_full_size_run(A, key):
         assert max_rel_err(ms_sel, r.v, sub_off, floor=MOM_FLOOR) < MOM_TOL
         for tau in whole:
             assert rel_err(var[:, tau], r.var[:, tau]) < VAR_TOL, tau
+
+
+def _period_means(steps, sync_t, N):
+    """V_t of eq. (vt): per period, the mean of Var[W_k] over its iterations
+    (0 right after a sync, the traced variance of the previous step otherwise)."""
+    syncs = set(int(t) for t in sync_t)
+    out, cur, after_sync = [], [], True
+    for t in range(N):
+        cur.append(0.0 if after_sync else steps["var"][t - 1])
+        after_sync = t in syncs
+        if after_sync:
+            out.append((t, float(np.mean(cur))))
+            cur = []
+    return out
+
+
+def _mean_in(series, lo, hi):
+    return float(np.mean([v for t, v in series if lo <= t < hi]))
+
+
+def test_full_size_variance_behaviour(A):
+    """The paper's Figs. 1-3 on the full ResNet18-shaped run (K = 8, P = 11.2M,
+    62 tensors, 2000 steps, 10x rate decays at steps 1000 and 1500): V_t under a
+    constant period 4 falls ~100x per decay (gamma^2, Section III-A); under
+    ADPSGD (p_init 4, K_s 500) p rises after each decay (Fig. 3) and V_t falls
+    ~10x (gamma, Section III-B), with fewer syncs."""
+    w = W.full_workloads()["resnet18_like"]
+    out = {}
+    for name, ww in (("cpsgd4", w.replace(period_mode=W.PERIOD_CONST, p_init=4, k_s=0)),
+                     ("adpsgd", w.replace(p_init=4))):
+        _say(f"full-size traced {name}")
+        with A.Adpsgd.from_workload(ww) as eng:
+            recs, _, n, steps = eng.run_traced(ww.total_steps, with_var=False)
+        out[name] = (recs, n, steps, _period_means(steps, recs["t"], ww.total_steps))
+    (_, n_cp, _, v_cp), (rec_ad, n_ad, st_ad, v_ad) = out["cpsgd4"], out["adpsgd"]
+    r_cp = _mean_in(v_cp, 600, 1000) / _mean_in(v_cp, 1100, 1500)
+    r_ad = _mean_in(v_ad, 600, 1000) / _mean_in(v_ad, 1100, 1500)
+    p = lambda lo, hi: rec_ad["p"][(rec_ad["t"] >= lo) & (rec_ad["t"] < hi)].mean()
+    _say(f"  V_t drop at the first decay: CPSGD {r_cp:.1f}x, ADPSGD {r_ad:.1f}x; ADPSGD mean p "
+         f"{p(500, 1000):.1f} / {p(1000, 1500):.1f} / {p(1500, 2000):.1f}; syncs {n_cp} vs {n_ad}")
+    assert 30 < r_cp < 300 and 3 < r_ad < 30 and r_ad < r_cp / 3
+    assert p(1000, 1500) > 2 * p(500, 1000) and p(1500, 2000) > p(1000, 1500)
+    assert n_ad < n_cp
+    gn = st_ad["grad_norm2"]
+    assert gn[-1] < gn[999] < gn[100] < gn[0]

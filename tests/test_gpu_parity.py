@@ -353,3 +353,42 @@ def test_separate_sync_averages_momentum(A, K):
     assert max_rel_err(m, r.v, off, floor=MOM_FLOOR) < MOM_TOL
     nz = np.diff(off) > 0
     assert rel_err(var[nz], var_o[nz]) < VAR_TOL
+
+
+# ---------------------------------------------------------------- traced runs
+
+def _traced_cases():
+    pw = W.parity_workloads()
+    return {
+        "resnet18_like": pw["resnet18_like"].replace(total_steps=1200, k_s=300),
+        "many_small": pw["many_small"].replace(total_steps=800, k_s=200),
+        "k3_const": _tiny(K=3, sizes=(5000, 3, 0, 5001), p_init=5, total_steps=60),
+        "vgg16_adaptive": pw["vgg16_adaptive"],
+    }
+
+
+@pytest.mark.parametrize("key", list(_traced_cases()))
+def test_traced_run_matches_oracle(A, key):
+    w = _traced_cases()[key]
+    _say(f"traced {key}: K={w.K} P={w.P} N={w.total_steps}")
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, var, n, steps = eng.run_traced(w.total_steps)
+    r = oracle.Oracle(w).run(trace=True)
+    assert np.array_equal(recs["t"], r.sync_t) and np.array_equal(recs["p"], r.sync_p)
+    assert np.array_equal(steps["t"], np.arange(w.total_steps))
+    assert np.array_equal(np.nonzero(steps["synced"])[0], r.sync_t)
+    ev, eg = rel_err(steps["var"], r.trace_var), rel_err(steps["grad_norm2"], r.trace_grad_norm2)
+    _say(f"  per-step variance err {ev:.2e}, gradient norm err {eg:.2e}")
+    assert ev < VAR_TOL and eg < VAR_TOL
+    np.testing.assert_array_equal(steps["var"][recs["t"]], recs["S"])
+
+
+@pytest.mark.parametrize("key", ["resnet18_like", "k3_const"])
+def test_traced_run_equals_plain_run(A, key):
+    import torch
+    w = _traced_cases()[key]
+    with A.Adpsgd.from_workload(w) as a, A.Adpsgd.from_workload(w) as b:
+        ra, va, na = a.run(w.total_steps)
+        rb, vb, nb, _ = b.run_traced(w.total_steps)
+        assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
+    assert na == nb and ra.tobytes() == rb.tobytes() and np.array_equal(va, vb)
