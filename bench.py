@@ -39,10 +39,11 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(w):
     """HBM bytes per local-step launch from the committed counter summary, if it
-    was taken on the current kernel sources; else None."""
-    if not os.path.exists(TRAFFIC_FILE):
+    was taken on the current kernel sources and this shape (K = 8, P = 138M);
+    else None."""
+    if (w.K, w.P) != (8, 138_000_000) or not os.path.exists(TRAFFIC_FILE):
         return None
     txt = open(TRAFFIC_FILE).read()
     m_d = re.search(r"kernel sources digest:\s*`?([0-9a-f]{16})", txt)
@@ -50,6 +51,33 @@ def measured_traffic():
     if not (m_d and m_b) or m_d.group(1) != kernel_source_digest():
         return None
     return float(m_b.group(1))
+
+
+def period_text(w) -> str:
+    import workloads as W
+    if w.period_mode == W.PERIOD_ADAPTIVE:
+        return f"adaptive, p_init {w.p_init}, K_s {w.k_s}, thresholds {w.thr_lo}/{w.thr_hi}"
+    kind = "Algorithm 1 offset" if w.period_mode == W.PERIOD_ALG1 else "constant"
+    return f"{kind} {w.p_init}"
+
+
+def copy_context(torch, n_bytes=2 << 30, reps=5):
+    """A plain device-to-device copy (torch's kernel) of n_bytes, as the
+    attainable-bandwidth context for the step kernels: GB/s counting the read
+    and the write."""
+    src = torch.ones(n_bytes // 4, device="cuda:0", dtype=torch.float32)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    return {"kernel": "torch copy_", "bytes_each_way": n_bytes, "avg_launch_ms": ms,
+            "achieved_GBs": 2 * n_bytes / (ms * 1e-3) / 1e9}
 
 
 def cpu_baseline(w, P_sample=16_000_000, steps=80):
@@ -133,6 +161,19 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     tm = eng.get_timing()
+    sep = None
+    if not args.no_timing:
+        # context outside the timed region: the separate sync (mean, broadcast and
+        # variance of all K rows, no step) that adpsgd_average runs
+        eng.set_timing(True)
+        for _ in range(5):
+            eng.average()
+        ta = eng.get_timing()
+        if ta.average_launches > 0:
+            a_ms = ta.average_ms / ta.average_launches
+            sep = {"avg_launch_ms": a_ms, "bytes_per_launch": 8 * w.K * w.P,
+                   "achieved_GBs": 8 * w.K * w.P / (a_ms * 1e-3) / 1e9,
+                   "segsum_avg_ms": ta.segsum_ms / max(ta.segsum_launches, 1)}
     eng.close()
 
     updates = w.K * w.P * N * args.steps
@@ -151,7 +192,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "K": w.K, "P": w.P, "T": w.T, "local_steps_per_run": N,
-                   "period": "adaptive, p_init 4, K_s 125, thresholds 0.7/1.3",
+                   "period": period_text(w),
                    "syncs_per_run": int(n_syncs[-1])},
     }
     if args.traced:
@@ -163,7 +204,7 @@ def main():
         step_ms = tm.step_ms / tm.step_launches
         achieved = step_bytes / (step_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w),
                            "kernel": "k_local_step", "bytes_per_launch": step_bytes,
                            "avg_launch_ms": step_ms}
         if tm.fused_launches > 0:
@@ -172,6 +213,10 @@ def main():
                                       "achieved_GBs": step_bytes / (fused_ms * 1e-3) / 1e9,
                                       "segsum_avg_ms": tm.segsum_ms / max(tm.segsum_launches, 1)}
         out["hbm_GBs_whole_run"] = (step_bytes * N * args.steps) / elapsed / 1e9
+    if sep:
+        out["separate_sync"] = sep
+    if not args.no_timing:
+        out["copy_context"] = copy_context(torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)
