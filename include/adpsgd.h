@@ -66,6 +66,16 @@ extern "C" {
 #define ADPSGD_PERIOD_ALG1 2     /* CPSGD with Algorithm 1's test: sync after every step t
                                     with t mod p == 0 (after steps 0, p, 2p, ...)           */
 
+/* ---- launch policies of adpsgd_run (adpsgd_set_launch_policy) ----------------- */
+#define ADPSGD_LAUNCH_HYBRID 0  /* default: steps the host can plan run as plain steps or
+                                   fused syncs; after a decisive sync the host waits for
+                                   its outcome while the GPU has queued work, else the
+                                   device decides the next steps itself                  */
+#define ADPSGD_LAUNCH_DEVICE 1  /* every step is decided on the device (step + optional
+                                   sync + reduction per step)                              */
+#define ADPSGD_LAUNCH_HOST 2    /* the host waits for every decision it needs; the device
+                                   only confirms syncs the host planned                    */
+
 typedef struct adpsgd_ctx adpsgd_ctx; /* opaque, owned by the library */
 
 /* Hyper-parameters (Algorithm 2's Require line: p_init, K_s; Section IV-A:
@@ -106,7 +116,8 @@ typedef struct {
     float *h;               /* [P] curvatures, written by init                               */
     float *xstar;           /* [P] optimum, written by init                                  */
     void *workspace;        /* >= adpsgd_workspace_bytes(...) bytes, 256-byte aligned;
-                               tile table, tile partials and the variance ring                */
+                               tile and chunk tables, partials, the device copy of the
+                               controller state and the record slots                       */
     size_t workspace_bytes;
     void *stream;           /* hipStream_t for every launch and copy; NULL = null stream     */
 } adpsgd_buffers;
@@ -154,7 +165,8 @@ typedef struct {
     double step_ms;     int64_t step_launches;     /* plain local step            */
     double fused_ms;    int64_t fused_launches;    /* last step of a period + sync */
     double average_ms;  int64_t average_launches;  /* separate mean/broadcast/var */
-    double segsum_ms;   int64_t segsum_launches;   /* per-tensor variance sums    */
+    double segsum_ms;   int64_t segsum_launches;   /* reduction: per-tensor sums and,
+                                                      in a run, the period decision */
     double trace_ms;    int64_t trace_launches;    /* traced plain step (step + variance) */
 } adpsgd_timing;
 
@@ -199,11 +211,15 @@ ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
 
 /* Run n_steps steps of Algorithm 2 from the current state: local steps, a sync
  * whenever adpsgd_sched_step says one is due (fused into that step), and the
- * controller after every sync.  log (host, log_cap records) and var_log (host,
- * [log_cap][T], may be NULL) receive the first log_cap syncs; *n_syncs (may be
- * NULL) the count of all syncs.  No sync is forced at the end.  Returns when
- * all enqueued work has finished.  On ENONFINITE the run stops at that sync;
- * steps already enqueued after it complete and are counted in the state. */
+ * controller after every sync.  Syncs whose outcome the host has not read back
+ * are decided on the device by the same rules in the same fp64 arithmetic, so
+ * the GPU does not wait for the host; the host replays every step and returns
+ * ESTATE if a device decision ever differs from its own.  log (host, log_cap
+ * records) and var_log (host, [log_cap][T], may be NULL) receive the first
+ * log_cap syncs; *n_syncs (may be NULL) the count of all syncs.  No sync is
+ * forced at the end.  Returns when all enqueued work has finished.  On
+ * ENONFINITE the run stops at that sync; steps already enqueued after it
+ * complete (with their syncs, logged) and are counted in the state. */
 ADPSGD_API int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
                double *var_log, int64_t *n_syncs);
 
@@ -222,6 +238,10 @@ ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
 /* Restore a state saved by adpsgd_get_state (x, m restored by the caller):
  * t >= 0, cnt >= 0, nC2 >= 0, 1 <= p <= p_max, C2 finite. */
 ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
+
+/* How adpsgd_run launches its steps (ADPSGD_LAUNCH_*); every policy computes the
+ * same results.  EINVAL for an unknown policy. */
+ADPSGD_API int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy);
 
 /* Per-kernel HIP-event timing (off by default).  Turning it on or reading it
  * waits for the stream. */

@@ -11,12 +11,13 @@ from typing import Optional
 import numpy as np
 
 from ._native import (  # noqa: F401
-    AdpsgdError, EDEVICE, EINVAL, ENONFINITE, ESTATE, EXPORTED, LIB_PATH, LR_CONST, LR_COSINE,
+    AdpsgdError, EDEVICE, EINVAL, ENONFINITE, ESTATE, EXPORTED, LAUNCH_DEVICE, LAUNCH_HOST, LAUNCH_HYBRID,
+    LIB_PATH, LR_CONST, LR_COSINE,
     LR_STEP, LR_WARMUP_STEP, OK, PERIOD_ADAPTIVE, PERIOD_ALG1, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
     adpsgd_get_state, adpsgd_get_timing, adpsgd_hparams, adpsgd_init, adpsgd_last_error,
     adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,
     adpsgd_run_traced, adpsgd_step_rec,
-    adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_state, adpsgd_set_timing,
+    adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_launch_policy, adpsgd_set_state, adpsgd_set_timing,
     adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
     make_hparams,
 )
@@ -99,6 +100,9 @@ class Adpsgd:
 
     def set_state(self, st: adpsgd_state) -> None:
         adpsgd_set_state(self.ctx, st)
+
+    def set_launch_policy(self, policy: int) -> None:
+        adpsgd_set_launch_policy(self.ctx, policy)
 
     def set_timing(self, on: bool) -> None:
         adpsgd_set_timing(self.ctx, on)

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libadpsgd.so")
 OK, EINVAL, ESTATE, EDEVICE, ENONFINITE = 0, -1, -2, -3, -4
 LR_CONST, LR_STEP, LR_COSINE, LR_WARMUP_STEP = 0, 1, 2, 3
 PERIOD_CONST, PERIOD_ADAPTIVE, PERIOD_ALG1 = 0, 1, 2
+LAUNCH_HYBRID, LAUNCH_DEVICE, LAUNCH_HOST = 0, 1, 2
 
 
 class AdpsgdError(RuntimeError):
@@ -92,6 +93,7 @@ _SIGS = {
                                     C.POINTER(adpsgd_step_rec), C.c_int64, _I64P]),
     "adpsgd_get_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
     "adpsgd_set_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
+    "adpsgd_set_launch_policy": (C.c_int, [_CTX, C.c_int32]),
     "adpsgd_set_timing": (C.c_int, [_CTX, C.c_int32]),
     "adpsgd_get_timing": (C.c_int, [_CTX, C.POINTER(adpsgd_timing)]),
     "adpsgd_destroy": (C.c_int, [_CTX]),
@@ -230,6 +232,10 @@ def adpsgd_get_state(ctx: int) -> adpsgd_state:
 
 def adpsgd_set_state(ctx: int, st: adpsgd_state) -> None:
     _check(lib.adpsgd_set_state(ctx, C.byref(st)))
+
+
+def adpsgd_set_launch_policy(ctx: int, policy: int) -> None:
+    _check(lib.adpsgd_set_launch_policy(ctx, policy))
 
 
 def adpsgd_set_timing(ctx: int, on: bool) -> None:

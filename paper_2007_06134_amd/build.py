@@ -44,7 +44,8 @@ def build(verbose: bool = False) -> str:
             objs.append(obj)
         for src in HOST_SOURCES:
             obj = os.path.join(tmp, src + ".o")
-            cmd = [cc, *COMMON, "-D__HIP_PLATFORM_AMD__", "-c", os.path.join(CSRC, src), "-o", obj]
+            # the host controller takes the same fp64 decisions as the device: no contraction
+            cmd = [cc, *COMMON, "-D__HIP_PLATFORM_AMD__", "-ffp-contract=off", "-c", os.path.join(CSRC, src), "-o", obj]
             _run(cmd, verbose)
             objs.append(obj)
         out_tmp = LIB + f".tmp{os.getpid()}"

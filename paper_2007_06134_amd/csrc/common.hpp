@@ -3,6 +3,7 @@
 #include <string>
 
 #include "adpsgd.h"
+#include "schedule.hpp"
 
 namespace adpsgd {
 
@@ -13,5 +14,7 @@ int ok();
 
 bool hparams_valid(const adpsgd_hparams *hp, std::string *why);
 int32_t p_max_of(const adpsgd_hparams *hp);
+// The schedule rules of hp, for period_at / sync_due / apply_sync.
+SchedRule rule_of(const adpsgd_hparams *hp);
 
 }  // namespace adpsgd

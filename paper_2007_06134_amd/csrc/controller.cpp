@@ -1,6 +1,7 @@
-// Host-only parts of ADPSGD: the learning-rate schedules and the adaptive
-// period controller (Algorithm 2, lines 1-3 and 13-19).  No HIP here, so the
-// controller runs and is tested without a GPU.
+// Host parts of ADPSGD: the learning-rate schedules and the adaptive period
+// controller (Algorithm 2, lines 1-3 and 13-19).  No device call here, so the
+// controller runs and is tested without a GPU; its rules are the inline
+// functions of schedule.hpp, which the device reduction kernel also uses.
 #include <algorithm>
 #include <climits>
 #include <cmath>
@@ -8,6 +9,7 @@
 
 #include "adpsgd.h"
 #include "common.hpp"
+#include "schedule.hpp"
 
 namespace adpsgd {
 
@@ -41,6 +43,19 @@ bool hparams_valid(const adpsgd_hparams *hp, std::string *why) {
 }
 
 int32_t p_max_of(const adpsgd_hparams *hp) { return hp->p_max > 0 ? hp->p_max : INT32_MAX; }
+
+SchedRule rule_of(const adpsgd_hparams *hp) {
+    SchedRule r{};
+    r.period_mode = hp->period_mode;
+    r.p_after = hp->p_after;
+    r.p_max = p_max_of(hp);
+    r.k_s = hp->k_s;
+    r.warmup = hp->sync_warmup_steps;
+    r.p_switch_step = hp->p_switch_step;
+    r.thr_lo = hp->thr_lo;
+    r.thr_hi = hp->thr_hi;
+    return r;
+}
 
 }  // namespace adpsgd
 
@@ -84,13 +99,11 @@ extern "C" int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st) {
 
 extern "C" int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int32_t *sync_due) {
     if (!hp || !st || !sync_due) return fail(ADPSGD_EINVAL, "NULL hparams, state or output");
+    const SchedRule r = rule_of(hp);
     const int64_t t = st->t;
     st->cnt += 1;
-    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE && hp->p_switch_step > 0 && t >= hp->p_switch_step)
-        st->p = hp->p_after;
-    if (t < hp->sync_warmup_steps) *sync_due = 1;
-    else if (hp->period_mode == ADPSGD_PERIOD_ALG1) *sync_due = (t % st->p) == 0;
-    else *sync_due = st->cnt >= st->p;
+    st->p = period_at(r, st->p, t);
+    *sync_due = adpsgd::sync_due(r, st->cnt, st->p, t) ? 1 : 0;
     st->t = t + 1;
     return ok();
 }
@@ -98,27 +111,14 @@ extern "C" int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int
 extern "C" int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
                                     double *margin) {
     if (!hp || !st) return fail(ADPSGD_EINVAL, "NULL hparams or state");
-    if (margin) *margin = std::numeric_limits<double>::quiet_NaN();
-    if (!std::isfinite(S)) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
-    st->cnt = 0;
-    if (hp->period_mode != ADPSGD_PERIOD_ADAPTIVE || t < hp->sync_warmup_steps) return ok();
-    const double gamma = adpsgd_lr(hp, t);
-    if (t < hp->k_s) {
-        // sampling phase: C2 is the running (cumulative) mean of S / gamma
-        st->nC2 += 1;
-        st->C2 += (S / gamma - st->C2) / (double)st->nC2;
-        return ok();
-    }
-    const double lo = hp->thr_lo * gamma * st->C2;
-    const double hi = hp->thr_hi * gamma * st->C2;
-    if (margin && lo > 0) {
-        const double m_lo = S / lo - 1.0, m_hi = S / hi - 1.0;
-        *margin = std::fabs(m_lo) < std::fabs(m_hi) ? m_lo : m_hi;
-    }
-    if (S < lo) {
-        if (st->p < p_max_of(hp)) st->p += 1;
-    } else if (S > hi) {
-        if (st->p > 1) st->p -= 1;
-    }
+    SchedState s{st->t, st->cnt, st->nC2, st->C2, st->p, 0};
+    double m = std::numeric_limits<double>::quiet_NaN();
+    const bool finite = apply_sync(rule_of(hp), t, adpsgd_lr(hp, t), S, &s, &m);
+    if (margin) *margin = m;
+    if (!finite) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
+    st->cnt = s.cnt;
+    st->nC2 = s.nC2;
+    st->C2 = s.C2;
+    st->p = s.p;
     return ok();
 }

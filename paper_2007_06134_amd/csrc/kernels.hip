@@ -9,15 +9,16 @@
 //                  mean; optionally fused behind the period's last local step
 //                  so a sync costs no extra pass over HBM.
 //   k_sync_loop    the same for a worker count without a compiled variant.
-//   k_seg_chunks,  fixed-order sums of the tile partials: per chunk of tiles,
-//   k_seg_tensors  then per tensor.
+//   k_reduce_chunks,  fixed-order sums of the tile partials per chunk, then
+//   k_reduce_finish   per tensor and over tensors, and Algorithm 2's period
+//                     decision when a run's schedule lives on the device.
 //
 // Work unit: a group of four consecutive elements of one worker's row, moved
 // with one dwordx4 load and store and fed by one Philox call.  On MI355X a
 // stream of one dwordx4 access per thread over a large grid sustains far more
 // HBM bandwidth than threads that each walk many rows, so every thread owns a
 // single (group, worker) pair.  The K threads of a group exchange replicas
-// through LDS at a sync.  No atomics and a fixed reduction order make results
+// through LDS at a sync.  No atomics and fixed reduction orders make results
 // bit-reproducible for a given (K, P, offsets).
 #include <cmath>
 
@@ -175,26 +176,39 @@ __device__ __forceinline__ f4 tree_sum_lds(const f4 (*rows)[64], int lane, int b
     }
 }
 
+// Step s.t of a run whose schedule lives on the device: does a sync follow
+// it?  Every thread reads the same state (written only by the reduction
+// kernel after a sync), so the answer is uniform over the launch.
+__device__ __forceinline__ bool device_due(const SyncParams &p) {
+    const SchedState s = *p.sched;
+    const int64_t t = (int64_t)p.s.t;
+    return sync_due(p.rule, s.cnt + (t - s.t) + 1, period_at(p.rule, s.p, t), t);
+}
+
 // One tile (at most 64 groups, one per lane) of one tensor.  Wave w owns the
 // rows k = w, w + W, ... (W = min(K, 16) waves, R = K / W rows each).  Each
 // thread steps its rows (modes with a step), publishes them in LDS, reads all
 // K rows of its lane back to form the mean in a fixed order (the same bits in
-// every thread), sums its squared deviations and, when averaging, writes the
-// mean over its rows (AVGM: the momentum rows too).  Tracing modes also sum
-// the squared gradient norm at the mean (wave 0 counts each element once).
-// partials[2 tile + {0, 1}] = (sum of squared deviations, gradient norm^2).
-// Lanes of groups cut by the tile bounds use masked scalar accesses.
+// every thread), sums its squared deviations and, when a sync is due, writes
+// the mean over its rows (with averaged momentum, the momentum rows too).  The
+// traced mode also sums the squared gradient norm at the mean (wave 0 counts
+// each element once).  partials[2 tile + {0, 1}] = (sum of squared
+// deviations, gradient norm^2).  In kDevice a step without a sync stores the
+// stepped rows and measures nothing.  Lanes of groups cut by the tile bounds
+// use masked scalar accesses.
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
 __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParams p) {
     constexpr int W = KT < 16 ? KT : 16;
     constexpr int R = KT / W;
     constexpr bool STEP = MODE != kAverage;
-    constexpr bool BCAST = MODE != kTrace;
-    constexpr bool GN = MODE == kTrace || MODE == kFusedTrace;
-    static_assert(!AVGM || BCAST, "momentum is averaged only by a sync");
+    constexpr bool GN = MODE == kDeviceTrace;
     __shared__ f4 rows[KT][64];
     __shared__ f4 mrows[AVGM ? KT : 1][64];
     const StepParams &a = p.s;
+    bool bcast = true;  // the host-decided modes always average
+    if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
+    const bool measure = MODE != kDevice || bcast;
+    const bool avg_m = AVGM && bcast;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const Tile tile = p.tiles[blockIdx.x];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
@@ -224,22 +238,25 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
             for (int r = 0; r < R; ++r) {
                 const int k = w + W * r;
                 sgd_update(a, xr[r], m[r], h, xs, step_noise(a, g, k));
-                if (!AVGM) {
+                if (!avg_m) {
                     float *mrow = a.m + (int64_t)k * a.P + e0;
                     if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
                 }
-                if (!BCAST) {     // tracing: the replicas keep their new values
+                if (!bcast) {     // no sync: the replicas keep their new values
                     float *xrow = a.x + (int64_t)k * a.P + e0;
                     if (full) st4<NT>(xrow, xr[r]); else st4_masked(xrow, xr[r], e0, lo, hi);
                 }
             }
         }
+        if (measure) {
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            rows[w + W * r][lane] = xr[r];
-            if (AVGM) mrows[w + W * r][lane] = m[r];
+            for (int r = 0; r < R; ++r) {
+                rows[w + W * r][lane] = xr[r];
+                if (AVGM) mrows[w + W * r][lane] = m[r];
+            }
         }
     }
+    if (!measure) return;  // uniform over the block
     __syncthreads();
     double acc = 0.0, gn = 0.0;
     if (active) {
@@ -249,12 +266,12 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
         for (int r = 0; r < R; ++r) {
             const f4 dk = mean - xr[r];
             dev2 = fma4(dk, dk, dev2);
-            if (BCAST) {
+            if (bcast) {
                 float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
                 if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
             }
         }
-        if (AVGM) {
+        if (avg_m) {
             const f4 mmean = tree_sum_lds<KT>(mrows, lane, 0) / splat((float)KT);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
@@ -274,17 +291,20 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
 }
 
 // Any K: one wave per tile, lane = group, the workers walked in a loop.  The
-// first pass sums the replicas (stepping and storing them in modes with a
-// step), the second re-reads them for the deviations and, when averaging,
-// writes the mean.  AVGM sums the momentum buffers in the first pass and
-// writes their mean in the second.
+// first pass steps and stores the replicas (modes with a step) and sums them;
+// the second re-reads them for the deviations and, when a sync is due, writes
+// the mean.  With averaged momentum the first pass also sums the momentum
+// buffers and the second writes their mean.  In kDevice a step without a sync
+// is the first pass alone.
 template <bool VEC, int MODE, bool AVGM>
 __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     constexpr bool STEP = MODE != kAverage;
-    constexpr bool BCAST = MODE != kTrace;
-    constexpr bool GN = MODE == kTrace || MODE == kFusedTrace;
-    static_assert(!AVGM || BCAST, "momentum is averaged only by a sync");
+    constexpr bool GN = MODE == kDeviceTrace;
     const StepParams &a = p.s;
+    bool bcast = true;
+    if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
+    const bool measure = MODE != kDevice || bcast;
+    const bool avg_m = AVGM && bcast;
     const Tile tile = p.tiles[blockIdx.x];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
     const int64_t g = (lo >> 2) + threadIdx.x;
@@ -307,29 +327,32 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             if (STEP) {
                 sgd_update(a, x, m, h, xs, step_noise(a, g, k));
                 if (full) st4<false>(xrow, x); else st4_masked(xrow, x, e0, lo, hi);
-                if (!AVGM) { if (full) st4<false>(mrow, m); else st4_masked(mrow, m, e0, lo, hi); }
+                if (!avg_m) { if (full) st4<false>(mrow, m); else st4_masked(mrow, m, e0, lo, hi); }
             }
             s = (k == 0) ? x : s + x;
             if (AVGM) sm = (k == 0) ? m : sm + m;
         }
-        const f4 mean = s / splat((float)a.K);
-        const f4 mmean = sm / splat((float)a.K);
-        f4 dev2 = splat(0.0f);
-        for (int k = 0; k < a.K; ++k) {
-            float *xrow = a.x + (int64_t)k * a.P + e0;
-            const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
-            const f4 dk = mean - x;
-            dev2 = fma4(dk, dk, dev2);
-            if (BCAST) { if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi); }
-            if (AVGM) {
-                float *mrow = a.m + (int64_t)k * a.P + e0;
-                if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
+        if (measure) {
+            const f4 mean = s / splat((float)a.K);
+            const f4 mmean = sm / splat((float)a.K);
+            f4 dev2 = splat(0.0f);
+            for (int k = 0; k < a.K; ++k) {
+                float *xrow = a.x + (int64_t)k * a.P + e0;
+                const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
+                const f4 dk = mean - x;
+                dev2 = fma4(dk, dk, dev2);
+                if (bcast) { if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi); }
+                if (avg_m) {
+                    float *mrow = a.m + (int64_t)k * a.P + e0;
+                    if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
+                }
             }
+            if (!full) dev2 = mask4(dev2, e0, lo, hi);
+            acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
+            if (GN) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
         }
-        if (!full) dev2 = mask4(dev2, e0, lo, hi);
-        acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
-        if (GN) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
+    if (!measure) return;
     const Pair total = block_sum2<1>(acc, gn);
     if (threadIdx.x == 0) {
         p.partials[2 * (int64_t)blockIdx.x] = total.a;
@@ -337,39 +360,159 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     }
 }
 
-// Level 1: the tiles of chunk c are [chunks[c].first, + count), all in one
-// tensor; both components of their partials are summed.
-__global__ void __launch_bounds__(kBlock) k_seg_chunks(const Chunk *chunks, const double *tile_partials,
-                                                      double *chunk_partials) {
-    const Chunk c = chunks[blockIdx.x];
+// ---------------------------------------------------------------- reduction
+
+__device__ __forceinline__ void write_hdr(const ReduceParams &r, int32_t due, int32_t p, int32_t p_next,
+                                          int32_t status, double S, double GN, const SchedState &st) {
+    SlotHdr h;
+    h.t = r.t;
+    h.due = due;
+    h.p = p;
+    h.p_next = p_next;
+    h.status = status;
+    h.S = S;
+    h.GN = GN;
+    h.C2 = st.C2;
+    h.nC2 = st.nC2;
+    *r.hdr = h;
+}
+
+// Is there a sync (or, when tracing, a step) to reduce?  Without a schedule
+// the caller decided there is one.  Uniform over a launch: the state changes
+// only at the end of k_reduce_finish.
+__device__ __forceinline__ bool reduce_due(const ReduceParams &r, int32_t *p_t, SchedState *st) {
+    *p_t = 0;
+    *st = SchedState{};
+    if (!r.sched) return true;
+    *st = *r.sched;
+    *p_t = period_at(r.rule, st->p, r.t);
+    return sync_due(r.rule, st->cnt + (r.t - st->t) + 1, *p_t, r.t);
+}
+
+// Level 1, one block per chunk: the chunk's tile partials, summed in a fixed
+// order (strided per thread, then the block tree).
+__global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
+    int32_t p_t;
+    SchedState st;
+    if (!reduce_due(r, &p_t, &st) && !r.traced) return;
+    const Chunk c = r.chunks[blockIdx.x];
     double a = 0.0, b = 0.0;
     for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) {
-        a += tile_partials[2 * (int64_t)(c.first + i)];
-        b += tile_partials[2 * (int64_t)(c.first + i) + 1];
+        a += r.tile_partials[2 * (int64_t)(c.first + i)];
+        b += r.tile_partials[2 * (int64_t)(c.first + i) + 1];
     }
-    const Pair total = block_sum2<kBlock / 64>(a, b);
+    const Pair cs = block_sum2<kBlock / 64>(a, b);
     if (threadIdx.x == 0) {
-        chunk_partials[2 * (int64_t)blockIdx.x] = total.a;
-        chunk_partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+        r.chunk_partials[2 * (int64_t)blockIdx.x] = cs.a;
+        r.chunk_partials[2 * (int64_t)blockIdx.x + 1] = cs.b;
     }
 }
 
-// Level 2, over tau's chunks [chunk_begin[tau], chunk_begin[tau+1]):
-// out[tau] = (sum of squared deviations) / K (the tensor's variance) and
-// out[T + tau] = its gradient norm^2.
-__global__ void __launch_bounds__(kBlock) k_seg_tensors(const int32_t *chunk_begin, const double *chunk_partials,
-                                                       double *out, int32_t T, int32_t K) {
-    const int32_t tau = blockIdx.x;
-    const int32_t b = chunk_begin[tau], e = chunk_begin[tau + 1];
-    double sa = 0.0, sb = 0.0;
-    for (int32_t i = b + (int32_t)threadIdx.x; i < e; i += kBlock) {
-        sa += chunk_partials[2 * (int64_t)i];
-        sb += chunk_partials[2 * (int64_t)i + 1];
+// Level 2 and the decision, one block.  Per-tensor sums of the chunk
+// partials, in a fixed order chosen by the tensor's chunk count: a tensor of
+// at most kSmallTensorChunks chunks is owned by one thread, which adds its
+// chunks from LDS (the partials pass through LDS in windows of kFinishWindow;
+// four interleaved partial sums, carried across windows in the device scratch
+// acc); a larger tensor is owned by one wave, whose lanes add strided chunks
+// from memory before a butterfly.  Then out[tau] = variance (deviation sum /
+// K), out[T + tau] = gradient norm^2; S and the norm total are block sums;
+// with a schedule, thread 0 applies Algorithm 2's lines 13-19 (the same
+// apply_sync as the host controller) and writes the new state.  out and the
+// record header are the host's pinned record slot, written directly; the
+// header is written in every case.
+constexpr int kFinishThreads = 256;
+constexpr int32_t kFinishWindow = 2048;
+__global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r) {
+    __shared__ double la[kFinishWindow], lb[kFinishWindow];
+    int32_t p_t;
+    SchedState st;
+    const bool due = reduce_due(r, &p_t, &st);
+    if (!due && !r.traced) {
+        if (threadIdx.x == 0) write_hdr(r, 0, p_t, p_t, ADPSGD_OK, 0.0, 0.0, st);
+        return;
     }
-    const Pair total = block_sum2<kBlock / 64>(sa, sb);
+    // small tensors: a thread each, from LDS
+    for (int32_t w0 = 0; w0 < r.n_chunks; w0 += kFinishWindow) {
+        const int32_t n = min(kFinishWindow, r.n_chunks - w0);
+        __syncthreads();  // the previous window has been consumed
+        for (int32_t i = (int32_t)threadIdx.x; i < n; i += kFinishThreads) {
+            la[i] = r.chunk_partials[2 * (int64_t)(w0 + i)];
+            lb[i] = r.chunk_partials[2 * (int64_t)(w0 + i) + 1];
+        }
+        __syncthreads();
+        for (int32_t tau = (int32_t)threadIdx.x; tau < r.T; tau += kFinishThreads) {
+            const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
+            if (ce - cb > kSmallTensorChunks) continue;
+            const int32_t b = max(cb, w0) - w0, e = min(ce, w0 + n) - w0;
+            if (b >= e) continue;
+            double a[4] = {0.0, 0.0, 0.0, 0.0}, g[4] = {0.0, 0.0, 0.0, 0.0};
+            int32_t i = b;
+            for (; i + 4 <= e; i += 4) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    a[j] += la[i + j];
+                    g[j] += lb[i + j];
+                }
+            }
+            if (i < e) { a[0] += la[i]; g[0] += lb[i]; }
+            if (i + 1 < e) { a[1] += la[i + 1]; g[1] += lb[i + 1]; }
+            if (i + 2 < e) { a[2] += la[i + 2]; g[2] += lb[i + 2]; }
+            double sa = (a[0] + a[1]) + (a[2] + a[3]), sg = (g[0] + g[1]) + (g[2] + g[3]);
+            if (w0 > cb) {  // continued from an earlier window
+                sa += r.acc[tau];
+                sg += r.acc[r.T + tau];
+            }
+            r.acc[tau] = sa;
+            r.acc[r.T + tau] = sg;
+        }
+    }
+    // large tensors (listed by the host): a wave each, from memory
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int32_t j = wave; j < r.n_large; j += kFinishThreads / 64) {
+        const int32_t tau = r.large[j];
+        const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
+        double a = 0.0, g = 0.0;
+        for (int32_t i = cb + lane; i < ce; i += 64) {
+            a += r.chunk_partials[2 * (int64_t)i];
+            g += r.chunk_partials[2 * (int64_t)i + 1];
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            a += __shfl_xor(a, off, 64);
+            g += __shfl_xor(g, off, 64);
+        }
+        if (lane == 0) {
+            r.acc[tau] = a;
+            r.acc[r.T + tau] = g;
+        }
+    }
+    __syncthreads();  // acc of the large tensors, for their owner threads below
+    double sa = 0.0, sb = 0.0;
+    for (int32_t tau = (int32_t)threadIdx.x; tau < r.T; tau += kFinishThreads) {
+        double v = 0.0, g = 0.0;
+        if (r.chunk_begin[tau + 1] > r.chunk_begin[tau]) {
+            v = r.acc[tau] / (double)r.K;
+            g = r.acc[r.T + tau];
+        }
+        r.out[tau] = v;
+        r.out[r.T + tau] = g;
+        sa += v;
+        sb += g;
+    }
+    const Pair tot = block_sum2<kFinishThreads / 64>(sa, sb);
     if (threadIdx.x == 0) {
-        out[tau] = total.a / (double)K;
-        out[T + tau] = total.b;
+        int32_t status = ADPSGD_OK, p_next = p_t;
+        if (r.sched && due) {
+            st.p = p_t;
+            if (apply_sync(r.rule, r.t, r.gamma, tot.a, &st, nullptr)) {
+                st.t = r.t + 1;
+                *r.sched = st;
+                p_next = st.p;
+            } else {
+                status = ADPSGD_ENONFINITE;
+            }
+        }
+        write_hdr(r, due ? 1 : 0, p_t, p_next, status, tot.a, tot.b, st);
     }
 }
 
@@ -424,9 +567,10 @@ hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool av
                                 : sync_dispatch<KT, kAverage, false>(p, n_tiles, vec, nt, st);
     case kFused: return avg_m ? sync_dispatch<KT, kFused, true>(p, n_tiles, vec, nt, st)
                               : sync_dispatch<KT, kFused, false>(p, n_tiles, vec, nt, st);
-    case kTrace: return sync_dispatch<KT, kTrace, false>(p, n_tiles, vec, nt, st);
-    default: return avg_m ? sync_dispatch<KT, kFusedTrace, true>(p, n_tiles, vec, nt, st)
-                          : sync_dispatch<KT, kFusedTrace, false>(p, n_tiles, vec, nt, st);
+    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true>(p, n_tiles, vec, nt, st)
+                               : sync_dispatch<KT, kDevice, false>(p, n_tiles, vec, nt, st);
+    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true>(p, n_tiles, vec, nt, st)
+                          : sync_dispatch<KT, kDeviceTrace, false>(p, n_tiles, vec, nt, st);
     }
 }
 
@@ -444,9 +588,10 @@ hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool av
                                 : loop_dispatch<kAverage, false>(p, n_tiles, vec, st);
     case kFused: return avg_m ? loop_dispatch<kFused, true>(p, n_tiles, vec, st)
                               : loop_dispatch<kFused, false>(p, n_tiles, vec, st);
-    case kTrace: return loop_dispatch<kTrace, false>(p, n_tiles, vec, st);
-    default: return avg_m ? loop_dispatch<kFusedTrace, true>(p, n_tiles, vec, st)
-                          : loop_dispatch<kFusedTrace, false>(p, n_tiles, vec, st);
+    case kDevice: return avg_m ? loop_dispatch<kDevice, true>(p, n_tiles, vec, st)
+                               : loop_dispatch<kDevice, false>(p, n_tiles, vec, st);
+    default: return avg_m ? loop_dispatch<kDeviceTrace, true>(p, n_tiles, vec, st)
+                          : loop_dispatch<kDeviceTrace, false>(p, n_tiles, vec, st);
     }
 }
 
@@ -469,7 +614,6 @@ hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,
                             hipStream_t st) {
     if (n_tiles <= 0) return hipSuccess;
-    if (mode == kTrace) avg_m = false;    // nothing is averaged without a sync
     switch (p.s.K) {
     case 1: return sync_dispatch<1>(p, n_tiles, mode, avg_m, vec, nt, st);
     case 2: return sync_dispatch<2>(p, n_tiles, mode, avg_m, vec, nt, st);
@@ -481,16 +625,13 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
     }
 }
 
-hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
-                         const double *tile_partials, double *chunk_partials, double *out, int32_t T, int32_t K,
-                         hipStream_t st) {
-    if (n_chunks > 0) {
-        k_seg_chunks<<<dim3((unsigned)n_chunks), dim3(kBlock), 0, st>>>(chunks, tile_partials, chunk_partials);
-        hipError_t e = hipGetLastError();
+hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {
+    if (r.n_chunks > 0) {
+        k_reduce_chunks<<<dim3((unsigned)r.n_chunks), dim3(kBlock), 0, st>>>(r);
+        const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (T <= 0) return hipSuccess;
-    k_seg_tensors<<<dim3((unsigned)T), dim3(kBlock), 0, st>>>(chunk_begin, chunk_partials, out, T, K);
+    k_reduce_finish<<<dim3(1), dim3(kFinishThreads), 0, st>>>(r);
     return hipGetLastError();
 }
 

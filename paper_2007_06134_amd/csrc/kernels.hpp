@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include "rng.hpp"
+#include "schedule.hpp"
 
 namespace adpsgd {
 
@@ -11,6 +12,7 @@ constexpr int kBlock = 256;          // threads per workgroup of the streaming k
 constexpr int64_t kTileElems = 256;  // sync tiles are cut at multiples of 256 elements,
                                      // so a tile spans at most 64 float4 groups (one wave)
 constexpr int32_t kChunkTiles = 1024;  // tiles per first-level chunk of the variance sum
+constexpr int32_t kSmallTensorChunks = 32;  // larger tensors are summed by a wave, not a thread
 
 // One sync tile: a contiguous element range inside one tensor.
 struct Tile {
@@ -23,6 +25,8 @@ struct Tile {
 struct Chunk {
     int32_t first;
     int32_t count;
+    int32_t tensor;
+    int32_t pad_;
 };
 
 // Everything a local step needs.  Replicas are rows of x/m with stride P.
@@ -40,32 +44,70 @@ struct StepParams {
 };
 
 struct SyncParams {
-    StepParams s;      // x, m, P, K; the step fields are used only when fused
+    StepParams s;      // x, m, P, K; the step fields are used by the modes with a step
     const Tile *tiles;
     double *partials;  // [2 n_tiles]: per tile, sum of sum_k (xbar - x_k)^2, gradient norm^2
+    // modes decided on the device: step s.t syncs iff Algorithm 2's counter,
+    // read from *sched at block start, says so (the state is written only by
+    // the reduction kernel that follows a sync)
+    const SchedState *sched;
+    SchedRule rule;
 };
 
 // Grid size of the local step for n_groups groups and K workers.
 int64_t local_step_blocks(int64_t n_groups, int32_t K);
 // vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4.
 hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, hipStream_t st);
-// What a sync-tile kernel does: average only (a separate sync), one local step
-// then average (a period's last step), one local step and only measure
-// (tracing: variance and gradient norm at the mean, replicas kept), or one
-// local step, measure and average (a traced period's last step).
-enum SyncMode : int { kAverage = 0, kFused = 1, kTrace = 2, kFusedTrace = 3 };
+// What a sync-tile kernel does:
+//   kAverage      average only (a separate sync);
+//   kFused        one local step, then average (a period's last step);
+//   kDevice       one local step, then average iff a sync is due (decided on
+//                 the device); without a sync nothing is measured;
+//   kDeviceTrace  one local step, measure (variance and gradient norm at the
+//                 mean), then average iff a sync is due.
+enum SyncMode : int { kAverage = 0, kFused = 1, kDevice = 2, kDeviceTrace = 3 };
 
 // Tile partials are pairs (sum of squared deviations, squared gradient norm at
-// the mean; the latter only in the tracing modes).  avg_m = true: a sync also
-// averages the momentum buffers.
+// the mean; the latter only when tracing).  avg_m = true: a sync also averages
+// the momentum buffers.
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec,
                             bool nontemporal, hipStream_t st);
-// chunk_partials[c] = sums of the tile partials of chunk c; then, over tau's
-// chunks [chunk_begin[tau], chunk_begin[tau+1]): out[tau] = variance
-// (deviation sum / K) and out[T + tau] = squared gradient norm.
-hipError_t launch_segsum(const Chunk *chunks, int64_t n_chunks, const int32_t *chunk_begin,
-                         const double *tile_partials, double *chunk_partials, double *out, int32_t T,
-                         int32_t K, hipStream_t st);
+
+// Record of one launch of the reduction kernel (one step or one sync).
+struct SlotHdr {
+    int64_t t;        // the step (or the sync's step)
+    int32_t due;      // 1: a sync followed the step
+    int32_t p;        // period in force for the step
+    int32_t p_next;   // period after the sync's decision
+    int32_t status;   // ADPSGD_OK, or ADPSGD_ENONFINITE when S was not finite
+    double S;         // sum over tensors of the variances (0 without a reduction)
+    double GN;        // sum over tensors of the gradient norms^2
+    double C2;        // controller state after the step
+    int64_t nC2;
+};
+constexpr size_t kSlotHdrBytes = 64;
+static_assert(sizeof(SlotHdr) <= kSlotHdrBytes, "slot header");
+
+struct ReduceParams {
+    const double *tile_partials;  // [2 n_tiles]
+    const Chunk *chunks;          // [n_chunks], in tensor order
+    const int32_t *chunk_begin;   // [T + 1]: chunks of tensor tau
+    double *chunk_partials;       // [2 n_chunks]
+    double *acc;                  // [2T] device scratch: per-tensor sums
+    const int32_t *large;         // [n_large] tensors of more than kSmallTensorChunks chunks
+    int32_t n_chunks, T, K, n_large;
+    double *out;                  // [2T]: variance per tensor, then gradient norm^2 (may be mapped host memory)
+    SlotHdr *hdr;                 // (may be mapped host memory)
+    SchedState *sched;            // non-null: the step's sync is decided and controlled here
+    SchedRule rule;
+    int64_t t;                    // the step
+    double gamma;                 // its rate in fp64 (Algorithm 2's gamma_t)
+    int32_t traced;               // reduce even when no sync is due
+};
+
+// Segmented fixed-order sums of the tile partials (chunks, then tensors, then
+// over tensors) and, with a schedule, Algorithm 2's lines 13-19 on the result.
+hipError_t launch_reduce(const ReduceParams &r, hipStream_t st);
 hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, double h_lo,
                                double h_hi, hipStream_t st);
 hipError_t launch_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0,

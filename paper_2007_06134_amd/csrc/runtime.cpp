@@ -1,6 +1,8 @@
 // Host runtime and C ABI of the ADPSGD hot path: argument validation, the tile
 // table of the segmented variance reduction, kernel launches on the caller's
-// stream, the pipelined Algorithm 2 driver, checkpoint state and timing.
+// stream, the Algorithm 2 driver (host-planned steps, device-decided syncs
+// where the host has not yet read a decision back), checkpoint state and
+// timing.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -31,8 +33,14 @@ int ok() {
 
 namespace {
 
-constexpr int kRing = 32;          // syncs whose variances may be in flight at once
-constexpr int kTimedMax = 1024;    // pending timed launches before a harvest
+constexpr int kRing = 32;          // record slots: launches with a reduction in flight at once
+constexpr int kTimedMax = 4096;    // pending timed launches before a harvest
+constexpr int64_t kMaxInflight = 1024;  // launched steps the host has not yet accounted for
+// The driver waits for an outstanding decision when at least this many steps
+// are queued behind it (the GPU stays busy meanwhile); otherwise it lets the
+// device decide, for at most kMaxUncertain steps in a row.
+constexpr int64_t kQueueToWait = 1;
+constexpr int kMaxUncertain = 2;
 constexpr int64_t kMaxK = 65536;
 constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
 
@@ -88,14 +96,18 @@ void build_plan(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::ve
         }
         const int32_t n = (int32_t)tiles->size() - first_tile;
         for (int32_t c = 0; c < n; c += kChunkTiles)
-            chunks->push_back(Chunk{first_tile + c, std::min(kChunkTiles, n - c)});
+            chunks->push_back(Chunk{first_tile + c, std::min(kChunkTiles, n - c), tau, 0});
     }
     (*chunk_begin)[T] = (int32_t)chunks->size();
 }
 
 struct Layout {
-    size_t tiles, chunks, chunk_begin, tile_partials, chunk_partials, var, total;
+    size_t tiles, chunks, chunk_begin, large, tile_partials, chunk_partials, acc, sched, total;
 };
+
+// A record slot (pinned host memory the reduction writes directly): the
+// header, then the T variances and the T gradient norms.
+size_t slot_bytes_for(int32_t T) { return align_up(kSlotHdrBytes + 2 * sizeof(double) * (size_t)T, 256); }
 
 Layout layout_for(const Plan &pl, int32_t T) {
     auto at_least_one = [](int64_t n) { return (size_t)std::max<int64_t>(n, 1); };
@@ -103,10 +115,12 @@ Layout layout_for(const Plan &pl, int32_t T) {
     l.tiles = 0;
     l.chunks = align_up(l.tiles + sizeof(Tile) * at_least_one(pl.n_tiles), 256);
     l.chunk_begin = align_up(l.chunks + sizeof(Chunk) * at_least_one(pl.n_chunks), 256);
-    l.tile_partials = align_up(l.chunk_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
+    l.large = align_up(l.chunk_begin + sizeof(int32_t) * (size_t)(T + 1), 256);
+    l.tile_partials = align_up(l.large + sizeof(int32_t) * (size_t)T, 256);
     l.chunk_partials = align_up(l.tile_partials + 2 * sizeof(double) * at_least_one(pl.n_tiles), 256);
-    l.var = align_up(l.chunk_partials + 2 * sizeof(double) * at_least_one(pl.n_chunks), 256);
-    l.total = align_up(l.var + sizeof(double) * (size_t)kRing * 2 * (size_t)T, 256);
+    l.acc = align_up(l.chunk_partials + 2 * sizeof(double) * at_least_one(pl.n_chunks), 256);
+    l.sched = align_up(l.acc + 2 * sizeof(double) * (size_t)T, 256);
+    l.total = align_up(l.sched + sizeof(SchedState), 256);
     return l;
 }
 
@@ -140,6 +154,7 @@ struct adpsgd_ctx {
     std::vector<Tile> tiles;
     std::vector<Chunk> chunks;
     std::vector<int32_t> chunk_begin;
+    std::vector<int32_t> large;     // tensors of more than kSmallTensorChunks chunks
     adpsgd_hparams hp{};
     adpsgd_buffers buf{};
     hipStream_t stream = nullptr;
@@ -147,17 +162,24 @@ struct adpsgd_ctx {
     Tile *d_tiles = nullptr;
     Chunk *d_chunks = nullptr;
     int32_t *d_chunk_begin = nullptr;
+    int32_t *d_large = nullptr;
     double *d_tile_partials = nullptr;
     double *d_chunk_partials = nullptr;
-    double *d_var = nullptr;        // [kRing][2T] device: variances, then gradient norms
-    double *h_var = nullptr;        // [kRing][2T] pinned host
+    double *d_acc = nullptr;        // [2T] reduction scratch
+    SchedState *d_sched = nullptr;  // the controller state as the device sees it during a run
+    char *h_slots = nullptr;        // [kRing] record slots: pinned, coherent host memory
+    char *d_slots = nullptr;        // the same slots as the device addresses them
+    SchedState *h_sched = nullptr;  // pinned staging for the device controller state
+    size_t slot_bytes = 0;
     hipEvent_t ring_ev[kRing] = {};
     adpsgd_state st{};
     bool vec = true;                // P % 4 == 0: dwordx4 rows
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
+    int32_t policy = ADPSGD_LAUNCH_HYBRID;
     RoundKeys rk{};
     bool timing = false;
     std::deque<TimedLaunch> timed;
+    int64_t timed_popped = 0;       // timed launches harvested so far (sequence of timed.front())
     std::vector<hipEvent_t> ev_pool;
     double t_ms[tKinds] = {};
     int64_t t_n[tKinds] = {};
@@ -174,7 +196,8 @@ void release(adpsgd_ctx *c) {
         (void)hipEventDestroy(tl.stop);
     }
     for (auto ev : c->ev_pool) (void)hipEventDestroy(ev);
-    if (c->h_var) (void)hipHostFree(c->h_var);
+    if (c->h_slots) (void)hipHostFree(c->h_slots);
+    if (c->h_sched) (void)hipHostFree(c->h_sched);
     delete c;
 }
 
@@ -188,30 +211,39 @@ int pool_event(adpsgd_ctx *c, hipEvent_t *ev) {
     return ok();
 }
 
-// Fold finished timed launches into the totals (all of them if wait_all).
+// Fold finished timed launches into the totals (all of them if wait_all).  A
+// launch whose kind is still open (-1: a device-decided step the driver has
+// not accounted for) stops a non-waiting harvest.
 int harvest(adpsgd_ctx *c, bool wait_all) {
     while (!c->timed.empty()) {
         TimedLaunch tl = c->timed.front();
         if (wait_all) {
             HIP_TRY(hipEventSynchronize(tl.stop));
         } else {
+            if (tl.kind < 0) break;
             hipError_t q = hipEventQuery(tl.stop);
             if (q == hipErrorNotReady) break;
             if (q != hipSuccess) return hip_fail(q, "hipEventQuery");
         }
         float ms = 0.f;
         HIP_TRY(hipEventElapsedTime(&ms, tl.start, tl.stop));
-        c->t_ms[tl.kind] += ms;
-        c->t_n[tl.kind] += 1;
+        const int kind = tl.kind < 0 ? tStep : tl.kind;
+        c->t_ms[kind] += ms;
+        c->t_n[kind] += 1;
         c->ev_pool.push_back(tl.start);
         c->ev_pool.push_back(tl.stop);
         c->timed.pop_front();
+        ++c->timed_popped;
     }
     return ok();
 }
 
+// Launch with HIP events around it when timing is on.  *seq (may be null)
+// receives the launch's sequence number, or -1 when it is not timed, for
+// set_timed_kind.
 template <class F>
-int timed_launch(adpsgd_ctx *c, int kind, F launch) {
+int timed_launch(adpsgd_ctx *c, int kind, F launch, int64_t *seq = nullptr) {
+    if (seq) *seq = -1;
     if (!c->timing) {
         HIP_TRY(launch());
         return ok();
@@ -232,8 +264,14 @@ int timed_launch(adpsgd_ctx *c, int kind, F launch) {
     HIP_TRY(hipEventRecord(tl.start, c->stream));
     HIP_TRY(launch());
     HIP_TRY(hipEventRecord(tl.stop, c->stream));
+    if (seq) *seq = c->timed_popped + (int64_t)c->timed.size();
     c->timed.push_back(tl);
     return ok();
+}
+
+void set_timed_kind(adpsgd_ctx *c, int64_t seq, int kind) {
+    const int64_t i = seq - c->timed_popped;
+    if (seq >= 0 && i >= 0 && i < (int64_t)c->timed.size()) c->timed[(size_t)i].kind = kind;
 }
 
 StepParams step_params(const adpsgd_ctx *c, int64_t t) {
@@ -263,28 +301,53 @@ int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
     return ok();
 }
 
-// A sync-tile kernel of the given mode at step t (the step is used by the
-// modes with a step), with its per-tensor variances (and gradient norms)
-// landing in ring slot `slot`.
-int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot) {
+SyncParams sync_params(const adpsgd_ctx *c, int64_t t) {
     SyncParams sp;
     sp.s = step_params(c, t);
     sp.tiles = c->d_tiles;
     sp.partials = c->d_tile_partials;
+    sp.sched = c->d_sched;
+    sp.rule = rule_of(&c->hp);
+    return sp;
+}
+
+char *slot_dev(const adpsgd_ctx *c, int slot) { return c->d_slots + (size_t)slot * c->slot_bytes; }
+const char *slot_host(const adpsgd_ctx *c, int slot) { return c->h_slots + (size_t)slot * c->slot_bytes; }
+
+// The sync-tile kernel of the given mode at step t, then the reduction into
+// record slot `slot` (with the controller on the device when ctl), then the
+// slot's event.  *step_seq: the timed sequence number of the tile kernel (its
+// kind is open for the device-decided modes).
+int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t *step_seq) {
+    const bool dev = mode == kDevice || mode == kDeviceTrace;
+    const SyncParams sp = sync_params(c, t);
     const int64_t n_tiles = (int64_t)c->tiles.size();
-    const int kind = mode == kAverage ? tAverage : mode == kTrace ? tTrace : tFused;
-    int rc = timed_launch(c, kind, [&] {
-        return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream);
-    });
+    const int kind = dev ? -1 : mode == kAverage ? tAverage : tFused;
+    int rc = timed_launch(
+        c, kind,
+        [&] { return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream); },
+        step_seq);
     if (rc) return rc;
-    double *dv = c->d_var + (size_t)slot * 2 * c->T;
-    rc = timed_launch(c, tSegsum, [&] {
-        return launch_segsum(c->d_chunks, (int64_t)c->chunks.size(), c->d_chunk_begin, c->d_tile_partials,
-                             c->d_chunk_partials, dv, c->T, c->K, c->stream);
-    });
+    ReduceParams r;
+    r.tile_partials = c->d_tile_partials;
+    r.chunks = c->d_chunks;
+    r.chunk_begin = c->d_chunk_begin;
+    r.chunk_partials = c->d_chunk_partials;
+    r.acc = c->d_acc;
+    r.n_chunks = (int32_t)c->chunks.size();
+    r.T = c->T;
+    r.K = c->K;
+    r.large = c->d_large;
+    r.n_large = (int32_t)c->large.size();
+    r.hdr = reinterpret_cast<SlotHdr *>(slot_dev(c, slot));
+    r.out = reinterpret_cast<double *>(slot_dev(c, slot) + kSlotHdrBytes);
+    r.sched = ctl ? c->d_sched : nullptr;
+    r.rule = sp.rule;
+    r.t = t;
+    r.gamma = adpsgd_lr(&c->hp, t);
+    r.traced = mode == kDeviceTrace ? 1 : 0;
+    rc = timed_launch(c, tSegsum, [&] { return launch_reduce(r, c->stream); });
     if (rc) return rc;
-    HIP_TRY(hipMemcpyAsync(c->h_var + (size_t)slot * 2 * c->T, dv, 2 * sizeof(double) * c->T,
-                           hipMemcpyDeviceToHost, c->stream));
     HIP_TRY(hipEventRecord(c->ring_ev[slot], c->stream));
     return ok();
 }
@@ -348,9 +411,14 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->d_tiles = (Tile *)(ws + lay.tiles);
     c->d_chunks = (Chunk *)(ws + lay.chunks);
     c->d_chunk_begin = (int32_t *)(ws + lay.chunk_begin);
+    c->d_large = (int32_t *)(ws + lay.large);
+    for (int32_t tau = 0; tau < T; ++tau)
+        if (c->chunk_begin[tau + 1] - c->chunk_begin[tau] > kSmallTensorChunks) c->large.push_back(tau);
     c->d_tile_partials = (double *)(ws + lay.tile_partials);
     c->d_chunk_partials = (double *)(ws + lay.chunk_partials);
-    c->d_var = (double *)(ws + lay.var);
+    c->d_acc = (double *)(ws + lay.acc);
+    c->d_sched = (SchedState *)(ws + lay.sched);
+    c->slot_bytes = slot_bytes_for(T);
 
     auto bail = [&](hipError_t e, const char *what) {
         int rc = hip_fail(e, what);
@@ -361,8 +429,13 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     };
     hipError_t e;
     if ((e = hipGetDevice(&c->device)) != hipSuccess) return bail(e, "hipGetDevice");
-    if ((e = hipHostMalloc((void **)&c->h_var, sizeof(double) * kRing * 2 * (size_t)T, hipHostMallocDefault)) !=
-        hipSuccess)
+    // the reduction writes its records straight into coherent pinned memory
+    if ((e = hipHostMalloc((void **)&c->h_slots, (size_t)kRing * c->slot_bytes,
+                           hipHostMallocMapped | hipHostMallocCoherent)) != hipSuccess)
+        return bail(e, "hipHostMalloc");
+    if ((e = hipHostGetDevicePointer((void **)&c->d_slots, c->h_slots, 0)) != hipSuccess)
+        return bail(e, "hipHostGetDevicePointer");
+    if ((e = hipHostMalloc((void **)&c->h_sched, sizeof(SchedState), hipHostMallocDefault)) != hipSuccess)
         return bail(e, "hipHostMalloc");
     for (auto &ev : c->ring_ev)
         if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) return bail(e, "hipEventCreate");
@@ -377,8 +450,10 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if ((e = hipMemcpyAsync(c->d_chunk_begin, c->chunk_begin.data(), sizeof(int32_t) * (T + 1),
                             hipMemcpyHostToDevice, c->stream)) != hipSuccess)
         return bail(e, "copy chunk offsets");
-    if ((e = hipMemsetAsync(c->d_var, 0, sizeof(double) * kRing * 2 * (size_t)T, c->stream)) != hipSuccess)
-        return bail(e, "clear variance ring");
+    if (!c->large.empty() &&
+        (e = hipMemcpyAsync(c->d_large, c->large.data(), sizeof(int32_t) * c->large.size(), hipMemcpyHostToDevice,
+                            c->stream)) != hipSuccess)
+        return bail(e, "copy large-tensor list");
     if (P > 0) {
         if ((e = launch_init_problem(buf->h, buf->xstar, P, hp->seed, hp->h_lo, hp->h_hi, c->stream)) != hipSuccess)
             return bail(e, "init_problem launch");
@@ -419,9 +494,9 @@ static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
     if (int rc = check_ctx(c)) return rc;
     if (!var_out) return fail(ADPSGD_EINVAL, "var_out is NULL");
     if (fused && c->st.t + 1 > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
-    if (int rc = enqueue_sync(c, fused ? kFused : kAverage, c->st.t, 0)) return rc;
+    if (int rc = enqueue_sync(c, fused ? kFused : kAverage, c->st.t, 0, false, nullptr)) return rc;
     HIP_TRY(hipEventSynchronize(c->ring_ev[0]));
-    std::memcpy(var_out, c->h_var, sizeof(double) * c->T);
+    std::memcpy(var_out, slot_host(c, 0) + kSlotHdrBytes, sizeof(double) * c->T);
     if (fused) c->st.t += 1;
     c->st.cnt = 0;
     return ok();
@@ -440,9 +515,20 @@ extern "C" int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
     return rc;
 }
 
-// Algorithm 2 for n_steps steps (adpsgd_run, adpsgd_run_traced).  With a
-// trace, every step takes a ring slot: plain steps run the tracing mode of the
-// sync-tile kernel, sync steps its traced fused mode.
+// Algorithm 2 for n_steps steps (adpsgd_run, adpsgd_run_traced).
+//
+// The host plans each step from its replay of the schedule: a step that ends
+// no period whatever the decisions still in flight runs the plain local step;
+// any other step runs the sync-tile kernel in a device-decided mode, which
+// steps and, iff Algorithm 2's counter (read from the device copy of the
+// controller state) says so, averages, followed by the reduction kernel that
+// sums the variances and applies lines 13-19 on the device.  After a decisive
+// sync the host waits for its outcome only while the GPU has queued steps
+// behind it; otherwise the device decides the next steps itself, so the GPU
+// never idles on a host round trip.  Every record is read back in order,
+// replayed by the host controller (same rules, same fp64 operations) and
+// checked against the device's decision.  A traced run sends every step
+// through the reduction.
 static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
                     adpsgd_step_rec *trace, int64_t trace_cap, int64_t *n_syncs) {
     if (int rc = check_ctx(c)) return rc;
@@ -452,87 +538,157 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
     if (c->st.t + n_steps > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
 
     const adpsgd_hparams &hp = c->hp;
-    const bool adaptive = hp.period_mode == ADPSGD_PERIOD_ADAPTIVE;
+    const SchedRule rule = rule_of(&hp);
     const bool traced = trace != nullptr;
-    const int64_t t0 = c->st.t, end = c->st.t + n_steps;
-    // plan: the schedule as enqueued on the stream (t, cnt, p).  c->st: the
-    // controller's view (p, C2, nC2), advanced as syncs are read back in order.
-    // They differ only while a decisive sync (one whose decision may move p) is
-    // in flight; then only steps that end no period under p - 1, p or p + 1
-    // are enqueued, so the GPU keeps working while the host waits.
-    adpsgd_state plan = c->st;
-    struct Pending { int64_t t; int32_t p; int slot; bool sync, decisive; };
-    std::deque<Pending> pend;
-    int64_t n_slots = 0, n_done = 0, lookahead = 0;
-    bool blocked = false;
+    const int64_t t0 = c->st.t, end = t0 + n_steps;
+
+    // The schedule from the host's point of view: exact, or the period known
+    // to lie in [lo, hi] (decisions in flight move p by at most one each), or
+    // unknown once a step whose sync the host could not predict is in flight.
+    struct Plan { bool exact; int64_t cnt; int32_t lo, hi; };
+    enum Cls { cPlain, cDue, cUncertain };
+    auto advance = [&](Plan &pl, int64_t t) -> Cls {
+        if (!pl.exact) return cUncertain;
+        pl.cnt += 1;
+        pl.lo = period_at(rule, pl.lo, t);
+        pl.hi = period_at(rule, pl.hi, t);
+        const bool due_lo = sync_due(rule, pl.cnt, pl.lo, t), due_hi = sync_due(rule, pl.cnt, pl.hi, t);
+        if (due_lo != due_hi) { pl.exact = false; return cUncertain; }
+        if (!due_lo) return cPlain;
+        pl.cnt = 0;
+        if (sync_decisive(rule, t)) {
+            pl.lo = std::max(pl.lo - 1, 1);
+            pl.hi = pl.hi < rule.p_max ? pl.hi + 1 : rule.p_max;
+        }
+        return cDue;
+    };
+
+    struct Entry { int64_t t; bool dev, uncertain; int slot; int64_t seq; };
+    std::deque<Entry> inflight;
+    adpsgd_state known = c->st;   // the host controller after every accounted step
+    Plan plan{true, known.cnt, known.p, known.p};
+    bool dirty = false;
+    int64_t launched = t0, n_done = 0, n_slots = 0;
+    int n_dev = 0, n_uncertain = 0;
     int status = ADPSGD_OK;
 
-    while (true) {
-        while (status == ADPSGD_OK && plan.t < end && (int)pend.size() < kRing && (!blocked || lookahead > 0)) {
-            const int64_t t = plan.t;
-            int32_t due = 0;
-            if ((status = adpsgd_sched_step(&hp, &plan, &due))) break;
-            if (blocked) {
-                // cnt <= max(p-1, 1) - 1 < p - 1: no period ends here for any p' >= p - 1
-                --lookahead;
-                if (due) { status = fail(ADPSGD_ESTATE, "internal: sync due inside the look-ahead"); break; }
-            }
-            if (!due && !traced) {
-                status = enqueue_steps(c, t, 1);
-                continue;
-            }
-            const int slot = (int)(n_slots % kRing);
-            const int mode = due ? (traced ? kFusedTrace : kFused) : kTrace;
-            if ((status = enqueue_sync(c, mode, t, slot))) break;
-            ++n_slots;
-            const bool decisive = due && adaptive && t >= hp.k_s && t >= hp.sync_warmup_steps;
-            pend.push_back(Pending{t, plan.p, slot, due != 0, decisive});
-            if (!due) continue;
-            plan.cnt = 0;
-            if (decisive) {
-                blocked = true;
-                lookahead = std::max(plan.p - 1, 1) - 1;
-            }
+    // Account for the front entry (finished, or a plain step): replay it on the
+    // host and check the device's record against the replay.
+    auto account = [&](const Entry &e) -> int {
+        int32_t due = 0;
+        (void)adpsgd_sched_step(&hp, &known, &due);
+        if (!e.dev) {
+            if (due) return fail(ADPSGD_ESTATE, "internal: a plain step ended a period");
+            return ADPSGD_OK;
         }
-        if (pend.empty() || status != ADPSGD_OK) break;
-        const Pending q = pend.front();
-        pend.pop_front();
-        hipError_t e = hipEventSynchronize(c->ring_ev[q.slot]);
-        if (e != hipSuccess) { status = hip_fail(e, "wait for variance"); break; }
-        const double *var = c->h_var + (size_t)q.slot * 2 * c->T;
-        const double S = sum_var(var, c->T);
-        if (traced && q.t - t0 < trace_cap)
-            trace[q.t - t0] = adpsgd_step_rec{q.t, q.sync ? 1 : 0, q.p, S, sum_var(var + c->T, c->T),
-                                              adpsgd_lr(&hp, q.t)};
-        if (q.sync) {
-            double margin = std::numeric_limits<double>::quiet_NaN();
-            const int rc = adpsgd_sched_on_sync(&hp, &c->st, q.t, S, &margin);
-            if (n_done < log_cap) {
-                log[n_done] = adpsgd_sync_rec{q.t, q.p, 0, S, c->st.C2, adpsgd_lr(&hp, q.t), margin};
-                if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
-            }
-            ++n_done;
-            if (rc) { status = rc; break; }
-            if (q.decisive) {
-                plan.p = c->st.p;
-                blocked = false;
-                lookahead = 0;
-            }
+        SlotHdr hdr;
+        std::memcpy(&hdr, slot_host(c, e.slot), sizeof hdr);
+        const double *var = reinterpret_cast<const double *>(slot_host(c, e.slot) + kSlotHdrBytes);
+        if (hdr.t != e.t || hdr.due != due)
+            return fail(ADPSGD_ESTATE, "device and host schedules disagree at step " + std::to_string(e.t));
+        set_timed_kind(c, e.seq, due ? tFused : traced ? tTrace : tStep);
+        const double gamma = adpsgd_lr(&hp, e.t);
+        if (traced && e.t - t0 < trace_cap)
+            trace[e.t - t0] = adpsgd_step_rec{e.t, due, known.p, hdr.S, hdr.GN, gamma};
+        if (!due) return ADPSGD_OK;
+        const int32_t p_in_force = known.p;
+        double margin = std::numeric_limits<double>::quiet_NaN();
+        const int rc = adpsgd_sched_on_sync(&hp, &known, e.t, hdr.S, &margin);
+        if (n_done < log_cap) {
+            log[n_done] = adpsgd_sync_rec{e.t, p_in_force, 0, hdr.S, known.C2, gamma, margin};
+            if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
         }
-        if (c->timing) {
-            int hr = harvest(c, false);
-            if (hr) { status = hr; break; }
+        ++n_done;
+        if (rc) return hdr.status == rc ? rc : fail(ADPSGD_ESTATE, "device and host disagree on a non-finite S");
+        if (hdr.status != ADPSGD_OK || hdr.p_next != known.p || hdr.C2 != known.C2 || hdr.nC2 != known.nC2)
+            return fail(ADPSGD_ESTATE, "device and host controllers disagree at step " + std::to_string(e.t));
+        return ADPSGD_OK;
+    };
+    // Account for every entry at the front that is finished (all of them,
+    // waiting, if wait_front: then at least the front one).
+    auto drain = [&](bool wait_front) -> int {
+        while (!inflight.empty()) {
+            const Entry e = inflight.front();
+            if (e.dev) {
+                hipError_t q = wait_front ? hipEventSynchronize(c->ring_ev[e.slot]) : hipEventQuery(c->ring_ev[e.slot]);
+                if (q == hipErrorNotReady) break;
+                if (q != hipSuccess) return hip_fail(q, "wait for a record");
+                wait_front = false;
+                --n_dev;
+                if (e.uncertain) --n_uncertain;
+                dirty = true;
+            }
+            inflight.pop_front();
+            const int rc = account(e);
+            // after a failure the remaining records are still accounted for
+            // (the steps ran); the first error is the one reported
+            if (rc && status == ADPSGD_OK) status = rc;
         }
+        return ADPSGD_OK;
+    };
+
+    if (n_steps > 0) {
+        *c->h_sched = SchedState{known.t, known.cnt, known.nC2, known.C2, known.p, 0};
+        HIP_TRY(hipMemcpyAsync(c->d_sched, c->h_sched, sizeof(SchedState), hipMemcpyHostToDevice, c->stream));
     }
-    // whatever was enqueued runs to completion; the state reflects it (on an
-    // error, p keeps the value in force before the failing sync)
+    int hard = ADPSGD_OK;  // a HIP failure: stop at once
+    while (hard == ADPSGD_OK) {
+        if ((hard = drain(false))) break;
+        if (c->timing && (hard = harvest(c, false))) break;
+        if (launched == end || status != ADPSGD_OK) {
+            if (inflight.empty()) break;
+            hard = drain(true);
+            continue;
+        }
+        if (dirty) {
+            plan = Plan{true, known.cnt, known.p, known.p};
+            for (const Entry &e : inflight) (void)advance(plan, e.t);
+            dirty = false;
+        }
+        Plan next = plan;
+        Cls cls = advance(next, launched);
+        if (traced || c->policy == ADPSGD_LAUNCH_DEVICE) cls = cDue;
+        bool wait = (int64_t)inflight.size() >= kMaxInflight || (cls != cPlain && n_dev >= kRing);
+        if (cls == cUncertain &&
+            (c->policy == ADPSGD_LAUNCH_HOST || (int64_t)inflight.size() - 1 >= kQueueToWait ||
+             n_uncertain >= kMaxUncertain))
+            wait = true;
+        if (wait) {
+            // the front entry is a device-decided one: plain entries are
+            // accounted for as soon as they reach the front (and with nothing
+            // in flight the plan is exact, so there is always something here)
+            if (inflight.empty()) { hard = fail(ADPSGD_ESTATE, "internal: nothing in flight to wait for"); break; }
+            hard = drain(true);
+            continue;
+        }
+        Entry e{launched, cls != cPlain, cls == cUncertain, -1, -1};
+        if (cls == cPlain) {
+            hard = enqueue_steps(c, launched, 1);
+        } else {
+            // a sync the host planned runs the fused kernel; the device's reduction
+            // still confirms it and takes the decision
+            const int mode = traced ? kDeviceTrace
+                                    : (cls == cDue && c->policy != ADPSGD_LAUNCH_DEVICE) ? kFused : kDevice;
+            e.slot = (int)(n_slots++ % kRing);
+            hard = enqueue_sync(c, mode, launched, e.slot, true, &e.seq);
+            ++n_dev;
+            if (e.uncertain) ++n_uncertain;
+        }
+        if (hard) break;
+        inflight.push_back(e);
+        plan = next;
+        ++launched;
+    }
+    // whatever was enqueued runs to completion and is accounted for
     hipError_t e = hipStreamSynchronize(c->stream);
-    c->st.t = plan.t;
-    c->st.cnt = plan.cnt;
-    if (!blocked) c->st.p = plan.p;
+    if (e == hipSuccess && hard == ADPSGD_OK) hard = drain(true);
+    if (e == hipSuccess && hard == ADPSGD_OK)
+        while (!inflight.empty() && hard == ADPSGD_OK) hard = drain(true);
+    c->st = known;
     if (n_syncs) *n_syncs = n_done;
-    if (status != ADPSGD_OK) return status;
+    if (hard != ADPSGD_OK) return hard;
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    if (status != ADPSGD_OK) return status;
     return ok();
 }
 
@@ -561,6 +717,14 @@ extern "C" int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in) {
         !std::isfinite(in->C2))
         return fail(ADPSGD_EINVAL, "invalid state");
     c->st = *in;
+    return ok();
+}
+
+extern "C" int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy) {
+    if (int rc = check_ctx(c)) return rc;
+    if (policy != ADPSGD_LAUNCH_HYBRID && policy != ADPSGD_LAUNCH_DEVICE && policy != ADPSGD_LAUNCH_HOST)
+        return fail(ADPSGD_EINVAL, "unknown launch policy");
+    c->policy = policy;
     return ok();
 }
 
