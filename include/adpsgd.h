@@ -160,7 +160,7 @@ typedef struct {
     double gamma;       /* learning rate of step t                                    */
 } adpsgd_step_rec;
 
-/* Per-kernel device time, from HIP events around each launch when enabled. */
+/* Per-kernel device time, from HIP events around the sampled launches. */
 typedef struct {
     double step_ms;     int64_t step_launches;     /* plain local step            */
     double fused_ms;    int64_t fused_launches;    /* last step of a period + sync */
@@ -243,9 +243,12 @@ ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
  * same results.  EINVAL for an unknown policy. */
 ADPSGD_API int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy);
 
-/* Per-kernel HIP-event timing (off by default).  Turning it on or reading it
- * waits for the stream. */
-ADPSGD_API int adpsgd_set_timing(adpsgd_ctx *c, int32_t on);
+/* Per-kernel HIP-event timing (off by default).  every = 0: off; every >= 1:
+ * HIP events around every every-th launch of each kernel kind (1: all), so the
+ * events disturb the timed work little; adpsgd_timing then holds the sampled
+ * launches.  Setting or reading it waits for the stream; setting it clears the
+ * totals.  EINVAL for every < 0. */
+ADPSGD_API int adpsgd_set_timing(adpsgd_ctx *c, int32_t every);
 ADPSGD_API int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out);
 
 /* Release the context (host memory and events).  Waits for the stream.  The

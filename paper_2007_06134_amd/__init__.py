@@ -104,8 +104,8 @@ class Adpsgd:
     def set_launch_policy(self, policy: int) -> None:
         adpsgd_set_launch_policy(self.ctx, policy)
 
-    def set_timing(self, on: bool) -> None:
-        adpsgd_set_timing(self.ctx, on)
+    def set_timing(self, every=True) -> None:
+        adpsgd_set_timing(self.ctx, every)
 
     def get_timing(self) -> adpsgd_timing:
         return adpsgd_get_timing(self.ctx)

@@ -238,8 +238,9 @@ def adpsgd_set_launch_policy(ctx: int, policy: int) -> None:
     _check(lib.adpsgd_set_launch_policy(ctx, policy))
 
 
-def adpsgd_set_timing(ctx: int, on: bool) -> None:
-    _check(lib.adpsgd_set_timing(ctx, 1 if on else 0))
+def adpsgd_set_timing(ctx: int, every) -> None:
+    """every: False/0 off, True/1 every launch, n > 1 every n-th launch of each kind."""
+    _check(lib.adpsgd_set_timing(ctx, int(every)))
 
 
 def adpsgd_get_timing(ctx: int) -> adpsgd_timing:

@@ -45,6 +45,9 @@ constexpr int64_t kMaxK = 65536;
 constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
 
 enum TimedKind { tStep = 0, tFused = 1, tAverage = 2, tSegsum = 3, tTrace = 4, tKinds = 5 };
+// Sampling classes of the timer: the timed kinds, plus the device-decided
+// step kernels whose kind is known only when their record is read.
+enum { cDeviceStep = tKinds, kTimedClasses = tKinds + 1 };
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -178,6 +181,8 @@ struct adpsgd_ctx {
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
     RoundKeys rk{};
     bool timing = false;
+    int32_t timing_every = 1;       // time every n-th launch of each class
+    int64_t class_count[kTimedClasses] = {};
     std::deque<TimedLaunch> timed;
     int64_t timed_popped = 0;       // timed launches harvested so far (sequence of timed.front())
     std::vector<hipEvent_t> ev_pool;
@@ -238,13 +243,15 @@ int harvest(adpsgd_ctx *c, bool wait_all) {
     return ok();
 }
 
-// Launch with HIP events around it when timing is on.  *seq (may be null)
-// receives the launch's sequence number, or -1 when it is not timed, for
-// set_timed_kind.
+// Launch, with HIP events around it when timing is on and this is the
+// sampled launch (every timing_every-th) of its class.  kind -1: decided later
+// (set_timed_kind).  *seq (may be null) receives the launch's sequence number,
+// or -1 when it is not timed.
 template <class F>
 int timed_launch(adpsgd_ctx *c, int kind, F launch, int64_t *seq = nullptr) {
     if (seq) *seq = -1;
-    if (!c->timing) {
+    const int cls = kind < 0 ? cDeviceStep : kind;
+    if (!c->timing || (c->class_count[cls]++ % c->timing_every) != 0) {
         HIP_TRY(launch());
         return ok();
     }
@@ -728,12 +735,15 @@ extern "C" int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy) {
     return ok();
 }
 
-extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t on) {
+extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t every) {
     if (int rc = check_ctx(c)) return rc;
+    if (every < 0) return fail(ADPSGD_EINVAL, "every must be >= 0");
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (int rc = harvest(c, true)) return rc;
-    c->timing = on != 0;
+    c->timing = every != 0;
+    c->timing_every = every > 0 ? every : 1;
     for (int i = 0; i < tKinds; ++i) { c->t_ms[i] = 0.0; c->t_n[i] = 0; }
+    for (auto &n : c->class_count) n = 0;
     return ok();
 }
 

@@ -259,6 +259,15 @@ def test_timing_counts_every_launch(A):
     assert tm.fused_launches == n and tm.segsum_launches >= n
     assert tm.step_launches == 100 - n and tm.average_launches == 0
     assert tm.step_ms > 0 and tm.fused_ms > 0
+    # sampled: events around every 4th launch of each kind
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.set_timing(4)
+        eng.run(100)
+        ts = eng.get_timing()
+        with pytest.raises(A.AdpsgdError):
+            eng.set_timing(-1)
+    assert 0 < ts.step_launches <= (100 - n + 3) // 4 + 2 and 0 < ts.fused_launches <= (n + 3) // 4 + 2
+    assert abs(ts.step_ms / ts.step_launches - tm.step_ms / tm.step_launches) < 0.5 * tm.step_ms / tm.step_launches
 
 
 # ---------------------------------------------------------------- edge cases and errors
