@@ -1,0 +1,80 @@
+// Host-side AddressSanitizer driver for the library's C ABI: every entry point,
+// every launch policy, traced runs, checkpoint state, timing, error paths.
+#include <hip/hip_runtime.h>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+#include <cmath>
+#include "adpsgd.h"
+
+#define CK(x) do { hipError_t e = (x); if (e != hipSuccess) { printf("HIP error %s at %d\n", hipGetErrorString(e), __LINE__); return 1;} } while(0)
+#define OKC(x) do { int rc = (x); if (rc != 0) { printf("adpsgd error %d (%s) at %d\n", rc, adpsgd_last_error(), __LINE__); return 1;} } while(0)
+
+static adpsgd_hparams hp_of(int mode, int p_init, int64_t N, int64_t k_s) {
+    adpsgd_hparams h{};
+    h.seed = 7; h.sigma = 0.1; h.momentum = 0.9; h.weight_decay = 5e-4; h.h_lo = 1e-2; h.h_hi = 1.0;
+    h.lr_kind = ADPSGD_LR_STEP; h.period_mode = mode; h.lr0 = 0.05; h.total_steps = N; h.p_init = p_init;
+    h.p_max = 0; h.k_s = k_s; h.thr_lo = 0.7; h.thr_hi = 1.3;
+    return h;
+}
+
+static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t N, int64_t k_s, int policy, bool traced) {
+    std::vector<int64_t> off(1, 0);
+    for (auto s : sizes) off.push_back(off.back() + s);
+    const int T = (int)sizes.size();
+    const int64_t P = off.back();
+    adpsgd_hparams hp = hp_of(mode, p_init, N, k_s);
+    size_t ws = adpsgd_workspace_bytes(K, P, T, off.data());
+    if (!ws) { printf("workspace 0\n"); return 1; }
+    float *x, *m, *h, *xs; void *w;
+    CK(hipMalloc(&x, 4 * (size_t)K * P + 16)); CK(hipMalloc(&m, 4 * (size_t)K * P + 16));
+    CK(hipMalloc(&h, 4 * (size_t)P + 16)); CK(hipMalloc(&xs, 4 * (size_t)P + 16)); CK(hipMalloc(&w, ws));
+    adpsgd_buffers b{x, m, h, xs, w, ws, nullptr};
+    adpsgd_ctx *c = nullptr;
+    OKC(adpsgd_init(K, P, off.data(), T, &hp, &b, &c));
+    OKC(adpsgd_set_launch_policy(c, policy));
+    OKC(adpsgd_set_timing(c, 3));
+    std::vector<adpsgd_sync_rec> log(N);
+    std::vector<double> var((size_t)N * T);
+    std::vector<adpsgd_step_rec> tr(N);
+    int64_t n = 0;
+    if (traced) OKC(adpsgd_run_traced(c, N / 2, log.data(), (int64_t)log.size(), var.data(), tr.data(), (int64_t)tr.size(), &n));
+    else OKC(adpsgd_run(c, N / 2, log.data(), (int64_t)log.size(), var.data(), &n));
+    adpsgd_state st;
+    OKC(adpsgd_get_state(c, &st));
+    // a small log capacity and no var log
+    OKC(adpsgd_run(c, N - N / 2, log.data(), 3, nullptr, &n));
+    OKC(adpsgd_set_state(c, &st));
+    std::vector<double> v(T);
+    OKC(adpsgd_local_steps(c, 3));
+    OKC(adpsgd_step_average(c, v.data()));
+    OKC(adpsgd_average(c, v.data()));
+    int32_t np = 0;
+    OKC(adpsgd_schedule(c, v.data(), &np));
+    adpsgd_timing tm;
+    OKC(adpsgd_get_timing(c, &tm));
+    // error paths leave the context usable
+    if (adpsgd_run(c, -1, nullptr, 0, nullptr, nullptr) != ADPSGD_EINVAL) { printf("expected EINVAL\n"); return 1; }
+    if (adpsgd_set_launch_policy(c, 9) != ADPSGD_EINVAL) { printf("expected EINVAL\n"); return 1; }
+    OKC(adpsgd_reset(c));
+    OKC(adpsgd_run(c, 5, nullptr, 0, nullptr, &n));
+    OKC(adpsgd_destroy(c));
+    CK(hipFree(x)); CK(hipFree(m)); CK(hipFree(h)); CK(hipFree(xs)); CK(hipFree(w));
+    printf("ok K=%d P=%lld T=%d mode=%d policy=%d traced=%d syncs=%lld timed steps=%lld\n", K, (long long)P, T, mode, policy,
+           (int)traced, (long long)n, (long long)tm.step_launches);
+    fflush(stdout);
+    return 0;
+}
+
+int main() {
+    const std::vector<int64_t> ragged = {5000, 77, 1, 0, 1024, 3, 70000, 263};
+    for (int policy = 0; policy < 3; ++policy)
+        for (int traced = 0; traced < 2; ++traced) {
+            if (one(8, ragged, ADPSGD_PERIOD_ADAPTIVE, 1, 120, 30, policy, traced)) return 1;
+            if (one(3, ragged, ADPSGD_PERIOD_ADAPTIVE, 2, 90, 20, policy, traced)) return 1;
+            if (one(32, {300000}, ADPSGD_PERIOD_CONST, 4, 40, 0, policy, traced)) return 1;
+            if (one(4, {0, 0}, ADPSGD_PERIOD_ALG1, 3, 20, 0, policy, traced)) return 1;
+        }
+    printf("all ok\n");
+    return 0;
+}
