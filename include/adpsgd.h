@@ -239,6 +239,14 @@ ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
  * t >= 0, cnt >= 0, nC2 >= 0, 1 <= p <= p_max, C2 finite. */
 ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
 
+/* Block size of the plain local step: 64, 128 or 256 threads (float4 groups of
+ * one worker's row per workgroup).  The fastest differs with the shape and the
+ * machine, so adpsgd_init times the three on the context's buffers when
+ * K * P >= 2^24 and keeps the fastest (else 256).  set: 64, 128 or 256, or 0 for
+ * the timed choice; every size computes the same bits.  EINVAL otherwise. */
+ADPSGD_API int adpsgd_set_step_block(adpsgd_ctx *c, int32_t block);
+ADPSGD_API int adpsgd_get_step_block(const adpsgd_ctx *c, int32_t *block);
+
 /* How adpsgd_run launches its steps (ADPSGD_LAUNCH_*); every policy computes the
  * same results.  EINVAL for an unknown policy. */
 ADPSGD_API int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy);

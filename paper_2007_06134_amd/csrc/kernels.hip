@@ -127,17 +127,19 @@ __device__ __forceinline__ double grad_norm2(const StepParams &a, f4 mean, f4 h,
 
 // ---------------------------------------------------------------- local step
 
-// Thread = (group g, worker k).  Blocks are ordered so that the K blocks of a
-// 256-group chunk are dispatched to the same XCD one after another (workgroups
-// go round-robin over the 8 XCDs): h and x* of the chunk come from HBM once and
-// from that XCD's L2 for the other K-1 workers.
-template <bool VEC, bool NT>
-__global__ void __launch_bounds__(kBlock) k_local_step(StepParams a) {
+// Thread = (group g, worker k); a block covers BS consecutive groups of one
+// worker's row.  Blocks are ordered so that the K blocks of a BS-group chunk
+// are dispatched to the same XCD one after another (workgroups go round-robin
+// over the 8 XCDs): h and x* of the chunk come from HBM once and from that
+// XCD's L2 for the other K-1 workers.  The best BS depends on the shape and
+// the machine (64, 128 and 256 each win somewhere); the runtime times them.
+template <int BS, bool VEC, bool NT>
+__global__ void __launch_bounds__(BS) k_local_step(StepParams a) {
     const int64_t b = blockIdx.x;
     const int64_t s = b >> 3;                        // position within the XCD
     const int k = (int)(s % a.K);
     const int64_t chunk = (s / a.K) * 8 + (b & 7);
-    const int64_t g = chunk * kBlock + threadIdx.x;
+    const int64_t g = chunk * BS + threadIdx.x;
     if (g >= a.n_groups) return;
     const int64_t e0 = 4 * g;
     float *xr = a.x + (int64_t)k * a.P + e0;
@@ -597,18 +599,28 @@ hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool av
 
 }  // namespace
 
-int64_t local_step_blocks(int64_t n_groups, int32_t K) {
-    const int64_t chunks = (n_groups + kBlock - 1) / kBlock;
+int64_t local_step_blocks(int64_t n_groups, int32_t K, int block) {
+    const int64_t chunks = (n_groups + block - 1) / block;
     return ((chunks + 7) / 8) * 8 * (int64_t)K;
 }
 
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, hipStream_t st) {
-    if (p.n_groups <= 0) return hipSuccess;
-    const dim3 grid((unsigned)local_step_blocks(p.n_groups, p.K)), block(kBlock);
-    if (vec && nt) k_local_step<true, true><<<grid, block, 0, st>>>(p);
-    else if (vec) k_local_step<true, false><<<grid, block, 0, st>>>(p);
-    else k_local_step<false, false><<<grid, block, 0, st>>>(p);
+template <int BS>
+hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, hipStream_t st) {
+    const dim3 grid((unsigned)local_step_blocks(p.n_groups, p.K, BS)), block(BS);
+    if (vec && nt) k_local_step<BS, true, true><<<grid, block, 0, st>>>(p);
+    else if (vec) k_local_step<BS, true, false><<<grid, block, 0, st>>>(p);
+    else k_local_step<BS, false, false><<<grid, block, 0, st>>>(p);
     return hipGetLastError();
+}
+
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, int block, hipStream_t st) {
+    if (p.n_groups <= 0) return hipSuccess;
+    switch (block) {
+    case 64: return local_step_bs<64>(p, vec, nt, st);
+    case 128: return local_step_bs<128>(p, vec, nt, st);
+    case 256: return local_step_bs<256>(p, vec, nt, st);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,

@@ -54,10 +54,13 @@ struct SyncParams {
     SchedRule rule;
 };
 
-// Grid size of the local step for n_groups groups and K workers.
-int64_t local_step_blocks(int64_t n_groups, int32_t K);
-// vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4.
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, hipStream_t st);
+// Block sizes of the local step (threads = groups per block), and its grid
+// size for n_groups groups, K workers and a block size.
+constexpr int kStepBlocks[] = {64, 128, 256};
+int64_t local_step_blocks(int64_t n_groups, int32_t K, int block);
+// vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4;
+// block: one of kStepBlocks (hipErrorInvalidValue otherwise).
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, int block, hipStream_t st);
 // What a sync-tile kernel does:
 //   kAverage      average only (a separate sync);
 //   kFused        one local step, then average (a period's last step);

@@ -41,6 +41,9 @@ constexpr int64_t kMaxInflight = 1024;  // launched steps the host has not yet a
 // device decide, for at most kMaxUncertain steps in a row.
 constexpr int64_t kQueueToWait = 1;
 constexpr int kMaxUncertain = 2;
+// adpsgd_init times the local step's block sizes when one step moves at least
+// this many elements (below it a launch is too short to time reliably).
+constexpr double kTuneMinElems = 16.0 * 1024 * 1024;
 constexpr int64_t kMaxK = 65536;
 constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
 
@@ -179,6 +182,8 @@ struct adpsgd_ctx {
     bool vec = true;                // P % 4 == 0: dwordx4 rows
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
+    int32_t step_block = 256;       // block size of the plain local step in use
+    int32_t tuned_block = 256;      // the fastest one measured at init
     RoundKeys rk{};
     bool timing = false;
     int32_t timing_every = 1;       // time every n-th launch of each class
@@ -302,7 +307,7 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
 int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
     for (int64_t j = 0; j < n; ++j) {
         const StepParams p = step_params(c, t0 + j);
-        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->stream); });
+        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->step_block, c->stream); });
         if (rc) return rc;
     }
     return ok();
@@ -370,6 +375,40 @@ int check_ctx(const adpsgd_ctx *c) {
     return ok();
 }
 
+// Time the local step at every block size on the context's own buffers (the
+// launches step x and m, which the caller zeroes afterwards): one warm-up
+// launch each, then three interleaved rounds; the fastest minimum wins.
+hipError_t tune_step_block(adpsgd_ctx *c) {
+    const StepParams p = step_params(c, 0);
+    constexpr int n = (int)(sizeof(kStepBlocks) / sizeof(kStepBlocks[0]));
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    float best[n];
+    for (int j = 0; j < n; ++j) best[j] = 3.4e38f;
+    for (int j = 0; j < n && e == hipSuccess; ++j) e = launch_local_step(p, c->vec, c->nontemporal, kStepBlocks[j], c->stream);
+    for (int round = 0; round < 3 && e == hipSuccess; ++round) {
+        for (int j = 0; j < n && e == hipSuccess; ++j) {
+            float ms = 0.f;
+            if ((e = hipEventRecord(a, c->stream)) != hipSuccess) break;
+            if ((e = launch_local_step(p, c->vec, c->nontemporal, kStepBlocks[j], c->stream)) != hipSuccess) break;
+            if ((e = hipEventRecord(b, c->stream)) != hipSuccess) break;
+            if ((e = hipEventSynchronize(b)) != hipSuccess) break;
+            if ((e = hipEventElapsedTime(&ms, a, b)) != hipSuccess) break;
+            best[j] = std::min(best[j], ms);
+        }
+    }
+    if (e == hipSuccess) {
+        int win = n - 1;
+        for (int j = 0; j < n; ++j)
+            if (best[j] < best[win]) win = j;
+        c->tuned_block = c->step_block = kStepBlocks[win];
+    }
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    return e;
+}
+
 }  // namespace
 
 extern "C" const char *adpsgd_last_error(void) { return g_last_error.c_str(); }
@@ -393,7 +432,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if (!aligned(buf->x, 16) || !aligned(buf->m, 16) || !aligned(buf->h, 16) || !aligned(buf->xstar, 16))
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be 16-byte aligned");
     const Plan plan = count_plan(T, offsets);
-    if (plan.n_tiles >= (int64_t(1) << 31) || local_step_blocks((P + 3) / 4, K) >= (int64_t(1) << 31))
+    if (plan.n_tiles >= (int64_t(1) << 31) || local_step_blocks((P + 3) / 4, K, kStepBlocks[0]) >= (int64_t(1) << 31))
         return fail(ADPSGD_EINVAL, "K * P too large for one launch");
     const Layout lay = layout_for(plan, T);
     if (!buf->workspace || !aligned(buf->workspace, 256)) return fail(ADPSGD_EINVAL, "workspace must be 256-byte aligned");
@@ -467,6 +506,11 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         const size_t bytes = sizeof(float) * (size_t)K * (size_t)P;
         if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
         if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
+        if ((double)K * (double)P >= kTuneMinElems) {
+            if ((e = tune_step_block(c)) != hipSuccess) return bail(e, "time the local step");
+            if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
+            if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
+        }
     }
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e, "hipStreamSynchronize");
     c->st = adpsgd_state{};
@@ -724,6 +768,23 @@ extern "C" int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in) {
         !std::isfinite(in->C2))
         return fail(ADPSGD_EINVAL, "invalid state");
     c->st = *in;
+    return ok();
+}
+
+extern "C" int adpsgd_set_step_block(adpsgd_ctx *c, int32_t block) {
+    if (int rc = check_ctx(c)) return rc;
+    if (block == 0) block = c->tuned_block;
+    bool known = false;
+    for (int b : kStepBlocks) known = known || b == block;
+    if (!known) return fail(ADPSGD_EINVAL, "block must be 0, 64, 128 or 256");
+    c->step_block = block;
+    return ok();
+}
+
+extern "C" int adpsgd_get_step_block(const adpsgd_ctx *c, int32_t *block) {
+    if (int rc = check_ctx(c)) return rc;
+    if (!block) return fail(ADPSGD_EINVAL, "block is NULL");
+    *block = c->step_block;
     return ok();
 }
 

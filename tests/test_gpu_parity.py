@@ -227,6 +227,28 @@ def test_launch_policies_agree_bitwise(A, key):
             (base["state"].t, base["state"].cnt, base["state"].p, base["state"].C2), pol
 
 
+def test_step_block_sizes_agree_bitwise(A):
+    """The plain local step at every block size (the init-time choice among
+    them depends on timing) computes the same bits."""
+    w = W.parity_workloads()["resnet18_like"].replace(total_steps=200, k_s=50)
+    runs = {}
+    for bs in (64, 128, 256):
+        with A.Adpsgd.from_workload(w) as eng:
+            eng.set_step_block(bs)
+            assert eng.step_block == bs
+            recs, var, n = eng.run(w.total_steps)
+            runs[bs] = (recs.tobytes(), var.tobytes(), eng.x.cpu().numpy().tobytes(), eng.m.cpu().numpy().tobytes())
+        with pytest.raises(A.AdpsgdError):
+            A.adpsgd_set_step_block(0, bs)   # a NULL context is refused
+    assert runs[64] == runs[128] == runs[256]
+    with A.Adpsgd.from_workload(w) as eng:
+        with pytest.raises(A.AdpsgdError) as e:
+            eng.set_step_block(96)
+        assert e.value.code == A.EINVAL
+        eng.set_step_block(0)
+        assert eng.step_block in (64, 128, 256)
+
+
 def test_checkpoint_resume_is_bit_exact(A):
     import torch
     w = W.parity_workloads()["resnet18_like"].replace(total_steps=700, k_s=150)
