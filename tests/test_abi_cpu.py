@@ -201,7 +201,7 @@ def _fake_buffers(A, ws=1 << 20, misalign=0):
 
 
 @pytest.mark.parametrize("K,offsets", [
-    (0, [0, 8]), (70000, [0, 8]), (2, [1, 8]), (2, [0, 9, 8]), (2, [0, 4, 9]),
+    (0, [0, 8]), (65537, [0, 8]), (2, [1, 8]), (2, [0, 9, 8]), (2, [0, 4, 9]),
 ])
 def test_init_rejects_bad_shapes(A, K, offsets):
     hp, _ = _hp(A)
@@ -231,6 +231,7 @@ def test_workspace_bytes_grows_with_tiles(A):
     many = A.adpsgd_workspace_bytes(8, 4096, list(range(0, 4097, 16)))
     assert 0 < small < big and small < many
     assert A.adpsgd_workspace_bytes(4, 0, [0, 0, 0]) > 0   # empty tensors are allowed
+    assert A.adpsgd_workspace_bytes(65536, 8, [0, 8]) > 0  # the largest worker count
 
 
 def test_null_context_and_dump_ranges(A):

@@ -162,3 +162,22 @@ def test_full_size_variance_behaviour(A):
     assert n_ad < n_cp
     gn = st_ad["grad_norm2"]
     assert gn[-1] < gn[999] < gn[100] < gn[0]
+
+
+def test_full_size_launch_policies_agree(A):
+    """The full ResNet18-shaped run (p = 1-2 for long stretches, so the default
+    driver lets the device decide many steps) gives the same bits when every
+    step is decided on the device and when the host waits for every decision."""
+    import torch
+    w = W.full_workloads()["resnet18_like"]
+    out = {}
+    for pol in (A.LAUNCH_HYBRID, A.LAUNCH_DEVICE, A.LAUNCH_HOST):
+        _say(f"full-size resnet18_like, launch policy {pol}")
+        with A.Adpsgd.from_workload(w) as eng:
+            eng.set_launch_policy(pol)
+            recs, var, n = eng.run(w.total_steps)
+            out[pol] = (recs.tobytes(), var.tobytes(), eng.x.clone(), eng.m.clone())
+    base = out[A.LAUNCH_HYBRID]
+    for pol, o in out.items():
+        assert o[0] == base[0] and o[1] == base[1], pol
+        assert torch.equal(o[2], base[2]) and torch.equal(o[3], base[3]), pol

@@ -294,6 +294,21 @@ def test_timing_counts_every_launch(A):
 
 # ---------------------------------------------------------------- edge cases and errors
 
+def test_maximum_worker_count(A):
+    """K = 65536, the most the library accepts, on a ragged 12-element vector:
+    the any-K sync kernel walks 65536 rows and the step grid has 524288 blocks."""
+    w = W.Workload(name="kmax", K=65536, sizes=(3, 9), seed=5, sigma=0.1, momentum=0.9,
+                   weight_decay=5e-4, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.05,
+                   total_steps=9, period_mode=W.PERIOD_CONST, p_init=4, k_s=0)
+    _say(f"maximum K: K={w.K} P={w.P}")
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    assert np.array_equal(g["recs"]["t"], r.sync_t)
+    assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
+    assert max_rel_err(g["x"], r.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(g["m"], r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
+
+
 def test_empty_parameter_vector(A):
     w = _tiny(K=4, sizes=(0, 0), p_init=3, total_steps=10)
     with A.Adpsgd.from_workload(w) as eng:
