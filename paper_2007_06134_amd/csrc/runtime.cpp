@@ -41,6 +41,9 @@ constexpr int64_t kMaxInflight = 1024;  // launched steps the host has not yet a
 // device decide, for at most kMaxUncertain steps in a row.
 constexpr int64_t kQueueToWait = 1;
 constexpr int kMaxUncertain = 2;
+// Between waits, the driver polls for finished records every kPollEvery launches
+// (each poll is a runtime call; plain steps need no accounting to proceed).
+constexpr int64_t kPollEvery = 8;
 // adpsgd_init times the local step's block sizes when one step moves at least
 // this many elements (below it a launch is too short to time reliably).
 constexpr double kTuneMinElems = 16.0 * 1024 * 1024;
@@ -684,8 +687,10 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
     }
     int hard = ADPSGD_OK;  // a HIP failure: stop at once
     while (hard == ADPSGD_OK) {
-        if ((hard = drain(false))) break;
-        if (c->timing && (hard = harvest(c, false))) break;
+        if ((launched - t0) % kPollEvery == 0) {
+            if ((hard = drain(false))) break;
+            if (c->timing && (hard = harvest(c, false))) break;
+        }
         if (launched == end || status != ADPSGD_OK) {
             if (inflight.empty()) break;
             hard = drain(true);
@@ -700,14 +705,20 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
         Cls cls = advance(next, launched);
         if (traced || c->policy == ADPSGD_LAUNCH_DEVICE) cls = cDue;
         bool wait = (int64_t)inflight.size() >= kMaxInflight || (cls != cPlain && n_dev >= kRing);
-        if (cls == cUncertain &&
-            (c->policy == ADPSGD_LAUNCH_HOST || (int64_t)inflight.size() - 1 >= kQueueToWait ||
-             n_uncertain >= kMaxUncertain))
-            wait = true;
+        if (cls == cUncertain && !wait) {
+            // steps queued on the GPU behind the oldest record not yet read
+            int64_t behind = 0;
+            bool seen_dev = false;
+            for (const Entry &q : inflight) {
+                if (seen_dev) ++behind;
+                seen_dev = seen_dev || q.dev;
+            }
+            wait = c->policy == ADPSGD_LAUNCH_HOST || behind >= kQueueToWait || n_uncertain >= kMaxUncertain;
+        }
         if (wait) {
-            // the front entry is a device-decided one: plain entries are
-            // accounted for as soon as they reach the front (and with nothing
-            // in flight the plan is exact, so there is always something here)
+            // account for the plain entries at the front and wait for the
+            // first device-decided one (with nothing in flight the plan is
+            // exact, so there is always something to wait for)
             if (inflight.empty()) { hard = fail(ADPSGD_ESTATE, "internal: nothing in flight to wait for"); break; }
             hard = drain(true);
             continue;
