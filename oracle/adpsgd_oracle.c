@@ -26,9 +26,18 @@
  *     sampling-phase syncs.
  *   - The sync test uses Algorithm 2's counter in both period modes; a constant
  *     period is Algorithm 2 without controller updates.
- *   - Momentum buffers are not averaged; only the parameters are.
+ *   - Momentum buffers are not averaged by default; only the parameters are
+ *     (avg_momentum = 1 averages them too, the other reading).
  *   - p never drops below 1.
  *   - The variance divides by K (not K-1) and sums over parameters.
+ *
+ * The paper's other strategies, as options of the same loop:
+ *   - a warm-up prefix that syncs after every step with no controller update
+ *     (the p = 1 warm-up of Sections III-B and IV-C);
+ *   - the gradual warm-up learning rate of Section IV-C;
+ *   - Algorithm 1's own test, sync when t mod p == 0;
+ *   - a constant period that changes at a given step (the two-phase strategies
+ *     of Section III-A and the decreasing period of Section V-B).
  *
  * Conventions the paper does not give (noise law and its generator):
  *   Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), key = (seed low 32 bits,
