@@ -416,14 +416,14 @@ __global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
 // chunks from LDS (the partials pass through LDS in windows of kFinishWindow;
 // four interleaved partial sums, carried across windows in the device scratch
 // acc); a larger tensor is owned by one wave, whose lanes add strided chunks
-// from memory before a butterfly.  Then out[tau] = variance (deviation sum /
+// (from LDS when all of them fit in one window, else from memory) before a
+// butterfly.  Then out[tau] = variance (deviation sum /
 // K), out[T + tau] = gradient norm^2; S and the norm total are block sums;
 // with a schedule, thread 0 applies Algorithm 2's lines 13-19 (the same
 // apply_sync as the host controller) and writes the new state.  out and the
 // record header are the host's pinned record slot, written directly; the
 // header is written in every case.
 constexpr int kFinishThreads = 256;
-constexpr int32_t kFinishWindow = 2048;
 __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r) {
     __shared__ double la[kFinishWindow], lb[kFinishWindow];
     int32_t p_t;
@@ -468,15 +468,17 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r
             r.acc[r.T + tau] = sg;
         }
     }
-    // large tensors (listed by the host): a wave each, from memory
+    // large tensors (listed by the host): a wave each, from LDS when every
+    // chunk partial fits in the one window, else from memory
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bool in_lds = r.n_chunks <= kFinishWindow;
     for (int32_t j = wave; j < r.n_large; j += kFinishThreads / 64) {
         const int32_t tau = r.large[j];
         const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
         double a = 0.0, g = 0.0;
         for (int32_t i = cb + lane; i < ce; i += 64) {
-            a += r.chunk_partials[2 * (int64_t)i];
-            g += r.chunk_partials[2 * (int64_t)i + 1];
+            a += in_lds ? la[i] : r.chunk_partials[2 * (int64_t)i];
+            g += in_lds ? lb[i] : r.chunk_partials[2 * (int64_t)i + 1];
         }
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1) {
@@ -638,7 +640,7 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
 }
 
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {
-    if (r.n_chunks > 0) {
+    if (r.n_chunks > 0 && !r.chunks_are_tiles) {
         k_reduce_chunks<<<dim3((unsigned)r.n_chunks), dim3(kBlock), 0, st>>>(r);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

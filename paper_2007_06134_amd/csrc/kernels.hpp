@@ -12,6 +12,11 @@ constexpr int kBlock = 256;          // threads per workgroup of the streaming k
 constexpr int64_t kTileElems = 256;  // sync tiles are cut at multiples of 256 elements,
                                      // so a tile spans at most 64 float4 groups (one wave)
 constexpr int32_t kChunkTiles = 1024;  // tiles per first-level chunk of the variance sum
+// Chunk partials the final reduction block holds in LDS at once.
+constexpr int32_t kFinishWindow = 2048;
+// Up to this many tiles (one LDS window), every tile is its own chunk: the tile
+// partials are the chunk partials and the first reduction launch is skipped.
+constexpr int64_t kDirectMaxTiles = kFinishWindow;
 constexpr int32_t kSmallTensorChunks = 32;  // larger tensors are summed by a wave, not a thread
 
 // One sync tile: a contiguous element range inside one tensor.
@@ -99,6 +104,8 @@ struct ReduceParams {
     double *acc;                  // [2T] device scratch: per-tensor sums
     const int32_t *large;         // [n_large] tensors of more than kSmallTensorChunks chunks
     int32_t n_chunks, T, K, n_large;
+    int32_t chunks_are_tiles;     // 1: chunk_partials is tile_partials (one tile per chunk)
+    int32_t pad_;
     double *out;                  // [2T]: variance per tensor, then gradient norm^2 (may be mapped host memory)
     SlotHdr *hdr;                 // (may be mapped host memory)
     SchedState *sched;            // non-null: the step's sync is decided and controlled here

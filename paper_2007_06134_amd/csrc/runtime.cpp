@@ -73,25 +73,27 @@ bool shape_valid(int32_t K, int64_t P, int32_t T, const int64_t *off, std::strin
 
 // Tiles: each tensor [a, b) is cut at multiples of kTileElems, so no tile
 // crosses a tensor boundary and a tile spans at most kTileElems / 4 groups.
-// Chunks: runs of at most kChunkTiles consecutive tiles of one tensor.
+// Chunks: runs of at most chunk_tiles consecutive tiles of one tensor, where
+// chunk_tiles is 1 for at most kDirectMaxTiles tiles (the tile partials then
+// serve as chunk partials) and kChunkTiles otherwise.
 int64_t tiles_of(int64_t a, int64_t b) { return b > a ? (b + kTileElems - 1) / kTileElems - a / kTileElems : 0; }
 
 struct Plan {
     int64_t n_tiles = 0, n_chunks = 0;
+    int32_t chunk_tiles = kChunkTiles;
 };
 
 Plan count_plan(int32_t T, const int64_t *off) {
     Plan pl;
-    for (int32_t tau = 0; tau < T; ++tau) {
-        const int64_t nt = tiles_of(off[tau], off[tau + 1]);
-        pl.n_tiles += nt;
-        pl.n_chunks += (nt + kChunkTiles - 1) / kChunkTiles;
-    }
+    for (int32_t tau = 0; tau < T; ++tau) pl.n_tiles += tiles_of(off[tau], off[tau + 1]);
+    pl.chunk_tiles = pl.n_tiles <= kDirectMaxTiles ? 1 : kChunkTiles;
+    for (int32_t tau = 0; tau < T; ++tau)
+        pl.n_chunks += (tiles_of(off[tau], off[tau + 1]) + pl.chunk_tiles - 1) / pl.chunk_tiles;
     return pl;
 }
 
-void build_plan(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::vector<Chunk> *chunks,
-                std::vector<int32_t> *chunk_begin) {
+void build_plan(int32_t T, const int64_t *off, int32_t chunk_tiles, std::vector<Tile> *tiles,
+                std::vector<Chunk> *chunks, std::vector<int32_t> *chunk_begin) {
     tiles->clear();
     chunks->clear();
     chunk_begin->assign(T + 1, 0);
@@ -104,8 +106,8 @@ void build_plan(int32_t T, const int64_t *off, std::vector<Tile> *tiles, std::ve
             s = e;
         }
         const int32_t n = (int32_t)tiles->size() - first_tile;
-        for (int32_t c = 0; c < n; c += kChunkTiles)
-            chunks->push_back(Chunk{first_tile + c, std::min(kChunkTiles, n - c), tau, 0});
+        for (int32_t c = 0; c < n; c += chunk_tiles)
+            chunks->push_back(Chunk{first_tile + c, std::min(chunk_tiles, n - c), tau, 0});
     }
     (*chunk_begin)[T] = (int32_t)chunks->size();
 }
@@ -172,6 +174,7 @@ struct adpsgd_ctx {
     Chunk *d_chunks = nullptr;
     int32_t *d_chunk_begin = nullptr;
     int32_t *d_large = nullptr;
+    bool chunks_are_tiles = false;  // every tile is its own chunk (small problems)
     double *d_tile_partials = nullptr;
     double *d_chunk_partials = nullptr;
     double *d_acc = nullptr;        // [2T] reduction scratch
@@ -347,7 +350,9 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     r.tile_partials = c->d_tile_partials;
     r.chunks = c->d_chunks;
     r.chunk_begin = c->d_chunk_begin;
-    r.chunk_partials = c->d_chunk_partials;
+    r.chunk_partials = c->chunks_are_tiles ? c->d_tile_partials : c->d_chunk_partials;
+    r.chunks_are_tiles = c->chunks_are_tiles ? 1 : 0;
+    r.pad_ = 0;
     r.acc = c->d_acc;
     r.n_chunks = (int32_t)c->chunks.size();
     r.T = c->T;
@@ -448,7 +453,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->P = P;
     c->T = T;
     c->offsets.assign(offsets, offsets + T + 1);
-    build_plan(T, offsets, &c->tiles, &c->chunks, &c->chunk_begin);
+    build_plan(T, offsets, plan.chunk_tiles, &c->tiles, &c->chunks, &c->chunk_begin);
+    c->chunks_are_tiles = plan.chunk_tiles == 1;
     c->hp = *hp;
     c->buf = *buf;
     c->stream = (hipStream_t)buf->stream;
