@@ -249,6 +249,48 @@ def test_step_block_sizes_agree_bitwise(A):
         assert eng.step_block in (64, 128, 256)
 
 
+def _random_workload(i):
+    """A seeded random small configuration: K (odd ones take the any-K sync
+    kernel), 1-11 ragged tensors (empty ones included), period mode, LR
+    schedule, warm-up prefix, period switch and momentum averaging."""
+    rng = np.random.default_rng(7000 + i)
+    K = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 12, 16, 24, 32]))
+    T = int(rng.integers(1, 12))
+    sizes = [int(s) for s in rng.integers(0, 6000, size=T)]
+    if sum(sizes) == 0:
+        sizes[-1] = 17
+    mode = int(rng.choice([W.PERIOD_CONST, W.PERIOD_ADAPTIVE, W.PERIOD_ALG1]))
+    N = int(rng.integers(24, 90))
+    kw = dict(name=f"random{i}", K=K, sizes=tuple(sizes), seed=100 + i,
+              sigma=float(rng.uniform(0.01, 0.3)), momentum=float(rng.choice([0.0, 0.5, 0.9])),
+              weight_decay=float(rng.choice([0.0, 1e-4, 5e-4])), h_lo=1e-2, h_hi=1.0,
+              lr_kind=int(rng.choice([W.LR_CONST, W.LR_STEP, W.LR_COSINE, W.LR_WARMUP_STEP])),
+              lr0=float(rng.uniform(0.01, 0.1)), total_steps=N, period_mode=mode,
+              p_init=int(rng.integers(1, 7)),
+              k_s=int(rng.integers(0, N // 2)) if mode == W.PERIOD_ADAPTIVE else 0,
+              sync_warmup_steps=int(rng.choice([0, 0, 4])), avg_momentum=bool(rng.integers(0, 2)))
+    if mode != W.PERIOD_ADAPTIVE and rng.integers(0, 2):
+        kw.update(p_switch_step=N // 2, p_after=int(rng.integers(1, 7)))
+    return W.Workload(**kw)
+
+
+@pytest.mark.parametrize("i", range(16))
+def test_random_workloads_match_oracle(A, i):
+    """Sixteen seeded random configurations against the oracle (x, m, the sync
+    list, S and the per-tensor variances).  Every decision of these seeds lies
+    more than 5% from a threshold in the oracle, far above fp32 rounding."""
+    w = _random_workload(i)
+    _say(f"random {i}: K={w.K} P={w.P} T={w.T} mode={w.period_mode} N={w.total_steps}")
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    assert np.array_equal(g["recs"]["t"], r.sync_t) and np.array_equal(g["recs"]["p"], r.sync_p)
+    assert rel_err(g["recs"]["S"], r.S, floor=1e-300) < VAR_TOL
+    assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
+    assert max_rel_err(g["x"], r.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(g["m"], r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
+    assert g["state"].t == w.total_steps and g["state"].p == r.state.p
+
+
 def test_checkpoint_resume_is_bit_exact(A):
     import torch
     w = W.parity_workloads()["resnet18_like"].replace(total_steps=700, k_s=150)
