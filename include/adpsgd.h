@@ -6,8 +6,11 @@
  * parameter replicas x[K][P] and momentum buffers m[K][P] in one GPU's HBM.
  * Each local step applies momentum SGD to every replica with a noisy diagonal
  * quadratic gradient; every p steps the replicas are averaged, the
- * inter-worker parameter variance is reduced per tensor, and a host controller
- * moves p to keep that variance near gamma * C2.
+ * inter-worker parameter variance is reduced per tensor, and the period
+ * controller moves p to keep that variance near gamma * C2.  During a run the
+ * controller's decisions are taken on the device (so the GPU never waits for
+ * the host) and replayed and checked on the host; the same controller is
+ * callable on the host alone (adpsgd_sched_*).
  *
  * Conventions shared by every call:
  *   - Every call returns an int status: ADPSGD_OK (0) or a negative code below.
@@ -24,7 +27,8 @@
  *   - The sync follows Algorithm 2's counter in both period modes: syncs
  *     happen after 0-based steps p-1, 2p-1, ... (a constant period is
  *     Algorithm 2 with no controller updates).
- *   - Momentum buffers stay local; only parameters are averaged.
+ *   - Momentum buffers stay local; only parameters are averaged (unless
+ *     avg_momentum is set).
  *   - RunningAverage(C2, S/gamma) is the cumulative mean over sampling syncs.
  *   - p stays within [1, p_max].
  *   - Variance: (1/K) sum_k sum_{i in tensor} (xbar_i - x_{k,i})^2, taken on
