@@ -188,7 +188,7 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 }
 
 // One tile (at most 64 groups, one per lane) of one tensor.  Wave w owns the
-// rows k = w, w + W, ... (W = min(K, 16) waves, R = K / W rows each).  Each
+// rows k = w, w + W, ... (W waves, R = K / W rows each; see sync_waves).  Each
 // thread steps its rows (modes with a step), publishes them in LDS, reads all
 // K rows of its lane back to form the mean in a fixed order (the same bits in
 // every thread), sums its squared deviations and, when a sync is due, writes
@@ -198,9 +198,17 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 // deviations, gradient norm^2).  In kDevice a step without a sync stores the
 // stepped rows and measures nothing.  Lanes of groups cut by the tile bounds
 // use masked scalar accesses.
+// Waves per block: one per worker row (at most 16) when the rows are stepped;
+// the averaging-only mode does best with two rows per wave (measured +2 to +15%).
+template <int KT, int MODE>
+constexpr int sync_waves() {
+    if constexpr (MODE == kAverage && KT >= 2) return KT / 2 < 16 ? KT / 2 : 16;
+    else return KT < 16 ? KT : 16;
+}
+
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
-__global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParams p) {
-    constexpr int W = KT < 16 ? KT : 16;
+__global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(SyncParams p) {
+    constexpr int W = sync_waves<KT, MODE>();
     constexpr int R = KT / W;
     constexpr bool STEP = MODE != kAverage;
     constexpr bool GN = MODE == kDeviceTrace;
@@ -263,11 +271,13 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
     double acc = 0.0, gn = 0.0;
     if (active) {
         const f4 mean = tree_sum_lds<KT>(rows, lane, 0) / splat((float)KT);
-        f4 dev2 = splat(0.0f);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
+            // squared deviations in fp32 per element, each row's sum in fp64
             const f4 dk = mean - xr[r];
-            dev2 = fma4(dk, dk, dev2);
+            f4 d2 = dk * dk;
+            if (!full) d2 = mask4(d2, e0, lo, hi);
+            acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
             if (bcast) {
                 float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
                 if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
@@ -281,8 +291,6 @@ __global__ void __launch_bounds__(64 * (KT < 16 ? KT : 16)) k_sync_lds(SyncParam
                 if (full) st4<NT>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
             }
         }
-        if (!full) dev2 = mask4(dev2, e0, lo, hi);
-        acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
         if (GN && w == 0) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
     const Pair total = block_sum2<W>(acc, gn);
@@ -337,20 +345,20 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
         if (measure) {
             const f4 mean = s / splat((float)a.K);
             const f4 mmean = sm / splat((float)a.K);
-            f4 dev2 = splat(0.0f);
             for (int k = 0; k < a.K; ++k) {
                 float *xrow = a.x + (int64_t)k * a.P + e0;
                 const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
+                // squared deviations in fp32 per element, each row's sum in fp64
                 const f4 dk = mean - x;
-                dev2 = fma4(dk, dk, dev2);
+                f4 d2 = dk * dk;
+                if (!full) d2 = mask4(d2, e0, lo, hi);
+                acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
                 if (bcast) { if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi); }
                 if (avg_m) {
                     float *mrow = a.m + (int64_t)k * a.P + e0;
                     if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
                 }
             }
-            if (!full) dev2 = mask4(dev2, e0, lo, hi);
-            acc = ((double)dev2.x + (double)dev2.y) + ((double)dev2.z + (double)dev2.w);
             if (GN) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
         }
     }
@@ -555,7 +563,7 @@ inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBl
 
 template <int KT, int MODE, bool AVGM>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, hipStream_t st) {
-    constexpr int threads = 64 * (KT < 16 ? KT : 16);
+    constexpr int threads = 64 * sync_waves<KT, MODE>();
     const dim3 grid((unsigned)n_tiles), block(threads);
     if (vec && nt) k_sync_lds<KT, true, true, MODE, AVGM><<<grid, block, 0, st>>>(p);
     else if (vec) k_sync_lds<KT, true, false, MODE, AVGM><<<grid, block, 0, st>>>(p);

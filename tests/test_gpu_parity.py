@@ -142,7 +142,9 @@ def test_fused_sync_equals_step_then_sync(A, K):
     with A.Adpsgd.from_workload(w) as a, A.Adpsgd.from_workload(w) as b:
         a.local_steps(4); va = a.step_average()
         b.local_steps(5); vb = b.average()
-        assert np.array_equal(va, vb)
+        # the replicas are bitwise equal (the same mean tree); the separate sync
+        # gives each wave two rows, so its variance sums round in another order
+        assert np.allclose(va, vb, rtol=1e-12, atol=0.0)
         assert a.get_state().t == b.get_state().t == 5
         import torch
         assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
