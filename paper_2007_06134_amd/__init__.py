@@ -134,3 +134,18 @@ class Adpsgd:
 
     def __exit__(self, *exc):
         self.close()
+
+
+def write_sync_log(path: str, recs: np.ndarray, var: Optional[np.ndarray] = None) -> int:
+    """Append one JSON line per sync record (t, p, S, C2, gamma, margin and, when
+    given, the per-tensor variances) to `path`; returns the number written."""
+    import json
+    with open(path, "a") as f:
+        for j, r in enumerate(recs):
+            row = {"t": int(r["t"]), "p": int(r["p"]), "S": float(r["S"]), "C2": float(r["C2"]),
+                   "gamma": float(r["gamma"]),
+                   "margin": None if np.isnan(r["margin"]) else float(r["margin"])}
+            if var is not None:
+                row["var"] = [float(v) for v in var[j]]
+            f.write(json.dumps(row) + "\n")
+    return len(recs)

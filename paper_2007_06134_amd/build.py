@@ -16,6 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libadpsgd.so")
 ARCH = "gfx950"
+ROCM_LIB = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "lib")   # roctx markers
 
 HIP_SOURCES = ["kernels.hip"]
 HOST_SOURCES = ["runtime.cpp", "controller.cpp"]
@@ -49,7 +50,8 @@ def build(verbose: bool = False) -> str:
             _run(cmd, verbose)
             objs.append(obj)
         out_tmp = LIB + f".tmp{os.getpid()}"
-        _run([cc, "-shared", f"--offload-arch={ARCH}", *objs, "-o", out_tmp], verbose)
+        _run([cc, "-shared", f"--offload-arch={ARCH}", *objs, "-L", ROCM_LIB, "-lrocprofiler-sdk-roctx",
+              f"-Wl,-rpath,{ROCM_LIB}", "-o", out_tmp], verbose)
         os.replace(out_tmp, LIB)
     return LIB
 

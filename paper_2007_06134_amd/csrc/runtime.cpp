@@ -5,13 +5,17 @@
 // timing.
 #include <hip/hip_runtime.h>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <deque>
 #include <limits>
+#include <mutex>
 #include <new>
 #include <string>
+#include <unordered_set>
 #include <vector>
 
 #include "adpsgd.h"
@@ -378,10 +382,25 @@ double sum_var(const double *v, int32_t T) {
     return s;
 }
 
+// Contexts created by adpsgd_init and not yet destroyed: a call with any other
+// pointer (a destroyed context, say) is refused instead of touching freed memory.
+std::mutex g_live_mu;
+std::unordered_set<const adpsgd_ctx *> g_live;
+
 int check_ctx(const adpsgd_ctx *c) {
     if (!c) return fail(ADPSGD_EINVAL, "context is NULL");
+    std::lock_guard<std::mutex> lock(g_live_mu);
+    if (!g_live.count(c)) return fail(ADPSGD_EINVAL, "not a live context (destroyed, or not made by adpsgd_init)");
     return ok();
 }
+
+// A roctx range for the duration of a call (visible with rocprofv3 --marker-trace).
+struct Range {
+    explicit Range(const char *name) { roctxRangePushA(name); }
+    ~Range() { roctxRangePop(); }
+    Range(const Range &) = delete;
+    Range &operator=(const Range &) = delete;
+};
 
 // Time the local step at every block size on the context's own buffers (the
 // launches step x and m, which the caller zeroes afterwards): one warm-up
@@ -429,6 +448,7 @@ extern "C" size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const 
 
 extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t T, const adpsgd_hparams *hp,
                            const adpsgd_buffers *buf, adpsgd_ctx **out) {
+    Range range_("adpsgd_init");
     std::string why;
     if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
     *out = nullptr;
@@ -524,6 +544,10 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e, "hipStreamSynchronize");
     c->st = adpsgd_state{};
     c->st.p = hp->p_init;
+    {
+        std::lock_guard<std::mutex> lock(g_live_mu);
+        g_live.insert(c);
+    }
     *out = c;
     return ok();
 }
@@ -541,6 +565,7 @@ extern "C" int adpsgd_reset(adpsgd_ctx *c) {
 }
 
 extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
+    Range range_("adpsgd_local_steps");
     if (int rc = check_ctx(c)) return rc;
     if (n < 0) return fail(ADPSGD_EINVAL, "n must be >= 0");
     if (c->st.t + n > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
@@ -551,6 +576,7 @@ extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
 }
 
 static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
+    Range range_("adpsgd_sync");
     if (int rc = check_ctx(c)) return rc;
     if (!var_out) return fail(ADPSGD_EINVAL, "var_out is NULL");
     if (fused && c->st.t + 1 > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
@@ -591,6 +617,7 @@ extern "C" int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
 // through the reduction.
 static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap, double *var_log,
                     adpsgd_step_rec *trace, int64_t trace_cap, int64_t *n_syncs) {
+    Range range_("adpsgd_run");
     if (int rc = check_ctx(c)) return rc;
     if (n_steps < 0 || log_cap < 0 || trace_cap < 0) return fail(ADPSGD_EINVAL, "n_steps and capacities must be >= 0");
     if (log_cap > 0 && !log) return fail(ADPSGD_EINVAL, "log is NULL with log_cap > 0");
@@ -670,7 +697,13 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
         while (!inflight.empty()) {
             const Entry e = inflight.front();
             if (e.dev) {
-                hipError_t q = wait_front ? hipEventSynchronize(c->ring_ev[e.slot]) : hipEventQuery(c->ring_ev[e.slot]);
+                hipError_t q;
+                if (wait_front) {
+                    Range wait_("adpsgd_run: wait for a record");
+                    q = hipEventSynchronize(c->ring_ev[e.slot]);
+                } else {
+                    q = hipEventQuery(c->ring_ev[e.slot]);
+                }
                 if (q == hipErrorNotReady) break;
                 if (q != hipSuccess) return hip_fail(q, "wait for a record");
                 wait_front = false;
@@ -838,6 +871,10 @@ extern "C" int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out) {
 
 extern "C" int adpsgd_destroy(adpsgd_ctx *c) {
     if (!c) return ok();
+    {
+        std::lock_guard<std::mutex> lock(g_live_mu);
+        if (!g_live.erase(c)) return fail(ADPSGD_EINVAL, "not a live context (destroyed twice?)");
+    }
     hipError_t e = hipStreamSynchronize(c->stream);
     release(c);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");

@@ -16,5 +16,5 @@ $HIPCC $FL $INC --offload-arch=gfx950 -ffp-contract=off -Xclang -target-feature 
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -ffp-contract=off -c "$SRC/runtime.cpp" -o "$OUT/runtime.o"
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -ffp-contract=off -c "$SRC/controller.cpp" -o "$OUT/controller.o"
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -c "$HERE/abi_asan_driver.cpp" -o "$OUT/driver.o"
-$HIPCC -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined --offload-arch=gfx950 "$OUT"/kernels.o "$OUT"/runtime.o "$OUT"/controller.o "$OUT"/driver.o -o "$OUT/abi_asan_driver"
+$HIPCC -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined --offload-arch=gfx950 "$OUT"/kernels.o "$OUT"/runtime.o "$OUT"/controller.o "$OUT"/driver.o -L/opt/rocm/lib -lrocprofiler-sdk-roctx -Wl,-rpath,/opt/rocm/lib -o "$OUT/abi_asan_driver"
 echo "$OUT/abi_asan_driver"

@@ -353,6 +353,45 @@ def test_maximum_worker_count(A):
     assert max_rel_err(g["m"], r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
 
 
+def test_sync_log_as_json_lines(A, tmp_path):
+    import json
+    w = _tiny(K=4, sizes=(4096, 3), p_init=4, total_steps=20, period_mode=W.PERIOD_ADAPTIVE, k_s=8)
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, var, n = eng.run(w.total_steps)
+    path = tmp_path / "syncs.jsonl"
+    assert A.write_sync_log(str(path), recs, var) == n == 5
+    rows = [json.loads(line) for line in path.read_text().splitlines()]
+    assert [r["t"] for r in rows] == list(recs["t"]) and rows[0]["margin"] is None
+    assert np.allclose([sum(r["var"]) for r in rows], recs["S"], rtol=1e-12)
+
+
+def test_destroyed_context_is_refused(A):
+    """A call with a destroyed context returns EINVAL instead of touching freed
+    memory, and a second destroy is refused."""
+    w = _tiny(K=2, sizes=(1024,))
+    eng = A.Adpsgd.from_workload(w)
+    raw = eng.ctx
+    eng.close()
+    lib = A._native.lib
+    assert lib.adpsgd_local_steps(raw, 1) == A.EINVAL
+    assert "not a live context" in A.adpsgd_last_error()
+    assert lib.adpsgd_destroy(raw) == A.EINVAL
+
+
+def test_divergence_surfaces_through_a_separate_sync(A):
+    """A diverging run: the separate sync reports non-finite variances and the
+    controller refuses them with ENONFINITE, p unchanged."""
+    w = _tiny(K=4, sizes=(4096,), lr0=50.0, p_init=5, total_steps=200,
+              period_mode=W.PERIOD_ADAPTIVE, k_s=0)
+    with A.Adpsgd.from_workload(w) as eng:
+        eng.local_steps(60)
+        var = eng.average()
+        assert not np.all(np.isfinite(var))
+        with pytest.raises(A.AdpsgdError) as e:
+            eng.schedule(var)
+        assert e.value.code == A.ENONFINITE and eng.get_state().p == 5
+
+
 def test_empty_parameter_vector(A):
     w = _tiny(K=4, sizes=(0, 0), p_init=3, total_steps=10)
     with A.Adpsgd.from_workload(w) as eng:
