@@ -20,7 +20,10 @@
  *   - Device buffers are caller-owned (the library never allocates or frees
  *     them).  Host arrays are read during the call and never retained, except
  *     where stated.
- *   - One context is used by one host thread at a time.
+ *   - One context is used by one host thread at a time.  A context pointer that
+ *     adpsgd_init did not return, or that was destroyed, is refused with
+ *     ADPSGD_EINVAL (so is a second adpsgd_destroy).
+ *   - The entry points are bracketed by roctx ranges (rocprofv3 --marker-trace).
  *   - Step indices t are 0-based: step t is the paper's iteration k = t.
  *
  * Readings of points the paper leaves open, used throughout:
