@@ -11,6 +11,7 @@ tests check, at full size, what it can compute one element at a time:
   per-tensor variance of every tensor it covers completely;
 * the controller's decisions, recomputed from the reported S values.
 """
+import os
 import sys
 
 import numpy as np
@@ -29,6 +30,7 @@ VAR_TOL = 1e-3
 # judged against max(|m|, rms of its tensor) instead of a 1e-2 rms floor.
 MOM_FLOOR = 1.0
 MOM_TOL = 10 * PARAM_TOL     # m integrates gradient errors with gain 1 / (1 - momentum)
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
 
 def _say(msg):
@@ -181,3 +183,36 @@ def test_full_size_launch_policies_agree(A):
     for pol, o in out.items():
         assert o[0] == base[0] and o[1] == base[1], pol
         assert torch.equal(o[2], base[2]) and torch.equal(o[3], base[3]), pol
+
+
+@pytest.mark.parametrize("key", ["resnet18_like"])
+def test_full_size_adaptive_run_matches_oracle(A, key):
+    """The whole adaptive run at full size, in the bench's launch configuration,
+    against the oracle's own full run (tests/golden/fullsize_<key>.npz, written
+    by tests/golden/make_fullsize_golden.py from the oracle alone): the same
+    sequence of sync steps and periods, S and the per-tensor variances within
+    1e-3, and the replicas and momenta at sampled elements."""
+    import torch
+    g = np.load(os.path.join(GOLDEN, f"fullsize_{key}.npz"))
+    w = W.full_workloads()[key]
+    _say(f"full size {key} against the oracle's full run ({len(g['sync_t'])} syncs)")
+    it = torch.from_numpy(g["idx"]).cuda()
+    rows = torch.from_numpy(g["rows"]).cuda()
+    with A.Adpsgd.from_workload(w) as eng:
+        recs, var, n = eng.run(w.total_steps)
+        xs_sel = eng.x.index_select(0, rows).index_select(1, it).double().cpu().numpy()
+        ms_sel = eng.m.index_select(0, rows).index_select(1, it).double().cpu().numpy()
+        st = eng.get_state()
+    assert n == len(g["sync_t"])
+    assert np.array_equal(recs["t"], g["sync_t"]), "sync steps differ"
+    assert np.array_equal(recs["p"], g["sync_p"])
+    assert rel_err(recs["S"], g["S"]) < VAR_TOL
+    assert rel_err(recs["C2"], g["C2"]) < VAR_TOL
+    assert rel_err(var[:20], g["var_head"]) < VAR_TOL
+    assert rel_err(var[-20:], g["var_tail"]) < VAR_TOL
+    sub_off = np.searchsorted(g["idx"], w.offsets())
+    ex = max_rel_err(xs_sel, g["x"], sub_off)
+    em = max_rel_err(ms_sel, g["v"], sub_off, floor=MOM_FLOOR)
+    _say(f"  {n} syncs identical; err x {ex:.2e} m {em:.2e} S {rel_err(recs['S'], g['S']):.2e}")
+    assert ex < PARAM_TOL and em < MOM_TOL
+    assert st.p == int(g["state_p"]) and st.nC2 == int(g["state_nC2"])
