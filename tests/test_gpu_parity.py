@@ -229,6 +229,45 @@ def test_launch_policies_agree_bitwise(A, key):
             (base["state"].t, base["state"].cnt, base["state"].p, base["state"].C2), pol
 
 
+@pytest.mark.parametrize("key,fused", [("resnet18_like", True), ("many_small", True),
+                                       ("quad_small", True), ("resnet18_like", False)])
+def test_manual_algorithm2_loop_equals_run(A, key, fused):
+    """Algorithm 2 driven by hand through the primitive calls (p - 1 local steps,
+    then the period's last step fused with the sync, or p local steps and a
+    separate sync; then the host scheduler on the returned variances) takes the
+    same syncs and computes the same replicas and momenta as adpsgd_run."""
+    w = W.parity_workloads()[key]
+    N = w.total_steps
+    _say(f"manual loop {key} fused={fused}: K={w.K} P={w.P} N={N}")
+    g = gpu_run(w)
+    t_list, p_list, S_list, var_list = [], [], [], []
+    with A.Adpsgd.from_workload(w) as eng:
+        p, t = w.p_init, 0
+        while t + p <= N:
+            if fused:
+                eng.local_steps(p - 1)
+                var = eng.step_average()
+            else:
+                eng.local_steps(p)
+                var = eng.average()
+            t_list.append(t + p - 1); p_list.append(p)
+            S_list.append(float(np.sum(var))); var_list.append(var)
+            t += p
+            p = eng.schedule(var)
+        eng.local_steps(N - t)
+        st = eng.get_state()
+        x = eng.x.double().cpu().numpy()
+        m = eng.m.double().cpu().numpy()
+    recs = g["recs"]
+    assert len(t_list) == g["n_syncs"]
+    assert np.array_equal(recs["t"], t_list) and np.array_equal(recs["p"], p_list)
+    assert np.array_equal(x, g["x"]) and np.array_equal(m, g["m"])
+    assert np.allclose(np.asarray(var_list), g["var"], rtol=1e-12, atol=0.0)
+    assert np.allclose(S_list, recs["S"], rtol=1e-12, atol=0.0)
+    assert (st.t, st.cnt, st.p, st.nC2) == (g["state"].t, g["state"].cnt, g["state"].p, g["state"].nC2)
+    assert st.C2 == pytest.approx(g["state"].C2, rel=1e-12)
+
+
 def test_step_block_sizes_agree_bitwise(A):
     """The plain local step at every block size (the init-time choice among
     them depends on timing) computes the same bits."""
