@@ -164,7 +164,7 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     tm = eng.get_timing()
-    step_block = eng.step_block
+    step_block, step_lds = eng.step_launch
     sep = None
     if not args.no_timing:
         # context outside the timed region: the separate sync (mean, broadcast and
@@ -209,7 +209,8 @@ def main():
         achieved = step_bytes / (step_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w),
-                           "kernel": f"k_local_step<{step_block}>", "bytes_per_launch": step_bytes,
+                           "kernel": f"k_local_step<{step_block}>",
+                           "lds_reserved_per_block": step_lds, "bytes_per_launch": step_bytes,
                            "avg_launch_ms": step_ms, "timed_launches": tm.step_launches,
                            "timed_every": args.timing_every}
         if tm.fused_launches > 0:

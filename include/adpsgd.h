@@ -185,7 +185,9 @@ ADPSGD_API size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const 
  * K >= 1 workers; P >= 0 parameters; T >= 1 tensors with host offsets[T+1],
  * non-decreasing, offsets[0] = 0, offsets[T] = P (empty tensors allowed).
  * Fills h and xstar from the seed, zeroes x and m, and waits for the stream.
- * P/4 and the step count must stay below 2^32 (Philox counter words). */
+ * P/4 and the step count must stay below 2^32 (Philox counter words).  Any
+ * K * P that fits the device is accepted: a kernel grid beyond what one
+ * dispatch holds (2^32 work-items) is issued as several launches. */
 ADPSGD_API int adpsgd_init(int32_t K, int64_t P, const int64_t *tensor_offsets, int32_t T,
                 const adpsgd_hparams *hp, const adpsgd_buffers *buf, adpsgd_ctx **out);
 
@@ -246,13 +248,17 @@ ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
  * t >= 0, cnt >= 0, nC2 >= 0, 1 <= p <= p_max, C2 finite. */
 ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
 
-/* Block size of the plain local step: 64, 128 or 256 threads (float4 groups of
- * one worker's row per workgroup).  The fastest differs with the shape and the
- * machine, so adpsgd_init times the three on the context's buffers when
- * K * P >= 2^24 and keeps the fastest (else 256).  set: 64, 128 or 256, or 0 for
- * the timed choice; every size computes the same bits.  EINVAL otherwise. */
-ADPSGD_API int adpsgd_set_step_block(adpsgd_ctx *c, int32_t block);
-ADPSGD_API int adpsgd_get_step_block(const adpsgd_ctx *c, int32_t *block);
+/* Launch shape of the plain local step: block = 64, 128 or 256 threads (float4
+ * groups of one worker's row per workgroup), and lds_bytes of LDS reserved per
+ * block, which the kernel does not use: it only holds each CU to
+ * floor(160 KB / lds_bytes) resident blocks (0: no reservation).  The fastest
+ * shape differs with the problem and the machine, so when K * P >= 2^24
+ * adpsgd_init times (64, 0), (64, 8192), (128, 0) and (256, 0) on the context's
+ * buffers and keeps the fastest (else (256, 0)).  set: block 64, 128 or 256 with
+ * lds_bytes in [0, 65536], or block 0 for the timed choice (lds_bytes ignored);
+ * every shape computes the same bits.  EINVAL otherwise. */
+ADPSGD_API int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes);
+ADPSGD_API int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes);
 
 /* How adpsgd_run launches its steps (ADPSGD_LAUNCH_*); every policy computes the
  * same results.  EINVAL for an unknown policy. */

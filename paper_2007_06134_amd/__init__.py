@@ -18,7 +18,7 @@ from ._native import (  # noqa: F401
     adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,
     adpsgd_run_traced, adpsgd_step_rec,
     adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_launch_policy, adpsgd_set_state, adpsgd_set_timing,
-    adpsgd_get_step_block, adpsgd_set_step_block,
+    adpsgd_get_step_launch, adpsgd_set_step_launch,
     adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
     make_hparams,
 )
@@ -103,11 +103,12 @@ class Adpsgd:
         adpsgd_set_state(self.ctx, st)
 
     @property
-    def step_block(self) -> int:
-        return adpsgd_get_step_block(self.ctx)
+    def step_launch(self) -> tuple:
+        """(threads per block, LDS bytes reserved per block) of the plain local step."""
+        return adpsgd_get_step_launch(self.ctx)
 
-    def set_step_block(self, block: int) -> None:
-        adpsgd_set_step_block(self.ctx, block)
+    def set_step_launch(self, block: int, lds_bytes: int = 0) -> None:
+        adpsgd_set_step_launch(self.ctx, block, lds_bytes)
 
     def set_launch_policy(self, policy: int) -> None:
         adpsgd_set_launch_policy(self.ctx, policy)

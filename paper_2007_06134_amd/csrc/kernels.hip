@@ -20,6 +20,7 @@
 // single (group, worker) pair.  The K threads of a group exchange replicas
 // through LDS at a sync.  No atomics and fixed reduction orders make results
 // bit-reproducible for a given (K, P, offsets).
+#include <algorithm>
 #include <cmath>
 
 #include "kernels.hpp"
@@ -135,7 +136,7 @@ __device__ __forceinline__ double grad_norm2(const StepParams &a, f4 mean, f4 h,
 // the machine (64, 128 and 256 each win somewhere); the runtime times them.
 template <int BS, bool VEC, bool NT>
 __global__ void __launch_bounds__(BS) k_local_step(StepParams a) {
-    const int64_t b = blockIdx.x;
+    const int64_t b = a.block0 + blockIdx.x;
     const int64_t s = b >> 3;                        // position within the XCD
     const int k = (int)(s % a.K);
     const int64_t chunk = (s / a.K) * 8 + (b & 7);
@@ -220,7 +221,8 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     const bool measure = MODE != kDevice || bcast;
     const bool avg_m = AVGM && bcast;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const Tile tile = p.tiles[blockIdx.x];
+    const int64_t ti = p.s.block0 + blockIdx.x;
+    const Tile tile = p.tiles[ti];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
     const int64_t g = (lo >> 2) + lane;
     const int64_t e0 = 4 * g;
@@ -295,8 +297,8 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     }
     const Pair total = block_sum2<W>(acc, gn);
     if (threadIdx.x == 0) {
-        p.partials[2 * (int64_t)blockIdx.x] = total.a;
-        p.partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+        p.partials[2 * ti] = total.a;
+        p.partials[2 * ti + 1] = total.b;
     }
 }
 
@@ -315,7 +317,8 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
     const bool measure = MODE != kDevice || bcast;
     const bool avg_m = AVGM && bcast;
-    const Tile tile = p.tiles[blockIdx.x];
+    const int64_t ti = p.s.block0 + blockIdx.x;
+    const Tile tile = p.tiles[ti];
     const int64_t lo = tile.start, hi = tile.start + tile.len;
     const int64_t g = (lo >> 2) + threadIdx.x;
     const int64_t e0 = 4 * g;
@@ -365,8 +368,8 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
     if (!measure) return;
     const Pair total = block_sum2<1>(acc, gn);
     if (threadIdx.x == 0) {
-        p.partials[2 * (int64_t)blockIdx.x] = total.a;
-        p.partials[2 * (int64_t)blockIdx.x + 1] = total.b;
+        p.partials[2 * ti] = total.a;
+        p.partials[2 * ti + 1] = total.b;
     }
 }
 
@@ -405,7 +408,8 @@ __global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
     int32_t p_t;
     SchedState st;
     if (!reduce_due(r, &p_t, &st) && !r.traced) return;
-    const Chunk c = r.chunks[blockIdx.x];
+    const int64_t ci = (int64_t)r.block0 + blockIdx.x;
+    const Chunk c = r.chunks[ci];
     double a = 0.0, b = 0.0;
     for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) {
         a += r.tile_partials[2 * (int64_t)(c.first + i)];
@@ -413,8 +417,8 @@ __global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
     }
     const Pair cs = block_sum2<kBlock / 64>(a, b);
     if (threadIdx.x == 0) {
-        r.chunk_partials[2 * (int64_t)blockIdx.x] = cs.a;
-        r.chunk_partials[2 * (int64_t)blockIdx.x + 1] = cs.b;
+        r.chunk_partials[2 * ci] = cs.a;
+        r.chunk_partials[2 * ci + 1] = cs.b;
     }
 }
 
@@ -531,8 +535,8 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r
 // ---------------------------------------------------------------- problem data
 
 __global__ void __launch_bounds__(kBlock) k_init_problem(float *h, float *xs, int64_t P, RoundKeys rk,
-                                                         float log_lo, float log_span) {
-    const int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+                                                         float log_lo, float log_span, int64_t g0) {
+    const int64_t g = g0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t e0 = 4 * g;
     if (e0 >= P) return;
     const u4 rh = philox10(u4{(uint32_t)g, 0u, 0u, TAG_CURVATURE}, rk);
@@ -561,14 +565,46 @@ __global__ void __launch_bounds__(kBlock) k_normal_dump(RoundKeys rk, uint32_t c
 
 inline unsigned blocks_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
 
+// Blocks of `threads` work-items that one launch may hold (a multiple of 8).
+constexpr int64_t piece_blocks(int threads) { return (kMaxLaunchItems / threads) & ~int64_t(7); }
+
+// launch(first block, block count) over [0, n_blocks) in pieces of at most
+// piece_blocks(threads) blocks.
+template <class F>
+hipError_t in_pieces(int64_t n_blocks, int threads, F launch) {
+    const int64_t step = piece_blocks(threads);
+    for (int64_t b0 = 0; b0 < n_blocks; b0 += step) {
+        launch(b0, (unsigned)std::min(step, n_blocks - b0));
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// The same for the element-wise kernels: launch(first group, group count) in
+// pieces of whole blocks of kBlock groups.
+template <class F>
+hipError_t groups_in_pieces(int64_t n, F launch) {
+    const int64_t step = piece_blocks(kBlock) * kBlock;
+    for (int64_t g0 = 0; g0 < n; g0 += step) {
+        const int64_t m = std::min(step, n - g0);
+        launch(g0, m, blocks_for(m));
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <int KT, int MODE, bool AVGM>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, hipStream_t st) {
     constexpr int threads = 64 * sync_waves<KT, MODE>();
-    const dim3 grid((unsigned)n_tiles), block(threads);
-    if (vec && nt) k_sync_lds<KT, true, true, MODE, AVGM><<<grid, block, 0, st>>>(p);
-    else if (vec) k_sync_lds<KT, true, false, MODE, AVGM><<<grid, block, 0, st>>>(p);
-    else k_sync_lds<KT, false, false, MODE, AVGM><<<grid, block, 0, st>>>(p);
-    return hipGetLastError();
+    return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
+        SyncParams q = p;
+        q.s.block0 = b0;
+        if (vec && nt) k_sync_lds<KT, true, true, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
+        else if (vec) k_sync_lds<KT, true, false, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
+        else k_sync_lds<KT, false, false, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
+    });
 }
 
 template <int KT>
@@ -588,10 +624,12 @@ hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool av
 
 template <int MODE, bool AVGM>
 hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, hipStream_t st) {
-    const dim3 grid((unsigned)n_tiles), block(64);
-    if (vec) k_sync_loop<true, MODE, AVGM><<<grid, block, 0, st>>>(p);
-    else k_sync_loop<false, MODE, AVGM><<<grid, block, 0, st>>>(p);
-    return hipGetLastError();
+    return in_pieces(n_tiles, 64, [&](int64_t b0, unsigned nb) {
+        SyncParams q = p;
+        q.s.block0 = b0;
+        if (vec) k_sync_loop<true, MODE, AVGM><<<dim3(nb), dim3(64), 0, st>>>(q);
+        else k_sync_loop<false, MODE, AVGM><<<dim3(nb), dim3(64), 0, st>>>(q);
+    });
 }
 
 hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, hipStream_t st) {
@@ -615,20 +653,24 @@ int64_t local_step_blocks(int64_t n_groups, int32_t K, int block) {
 }
 
 template <int BS>
-hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, hipStream_t st) {
-    const dim3 grid((unsigned)local_step_blocks(p.n_groups, p.K, BS)), block(BS);
-    if (vec && nt) k_local_step<BS, true, true><<<grid, block, 0, st>>>(p);
-    else if (vec) k_local_step<BS, true, false><<<grid, block, 0, st>>>(p);
-    else k_local_step<BS, false, false><<<grid, block, 0, st>>>(p);
-    return hipGetLastError();
+hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, int lds, hipStream_t st) {
+    // lds: dynamic LDS per block that the kernel never touches (an occupancy cap)
+    return in_pieces(local_step_blocks(p.n_groups, p.K, BS), BS, [&](int64_t b0, unsigned nb) {
+        StepParams q = p;
+        q.block0 = b0;
+        if (vec && nt) k_local_step<BS, true, true><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else if (vec) k_local_step<BS, true, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else k_local_step<BS, false, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
+    });
 }
 
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, int block, hipStream_t st) {
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, int block, int lds, hipStream_t st) {
+    if (lds < 0 || lds > kMaxStepLds) return hipErrorInvalidValue;
     if (p.n_groups <= 0) return hipSuccess;
     switch (block) {
-    case 64: return local_step_bs<64>(p, vec, nt, st);
-    case 128: return local_step_bs<128>(p, vec, nt, st);
-    case 256: return local_step_bs<256>(p, vec, nt, st);
+    case 64: return local_step_bs<64>(p, vec, nt, lds, st);
+    case 128: return local_step_bs<128>(p, vec, nt, lds, st);
+    case 256: return local_step_bs<256>(p, vec, nt, lds, st);
     default: return hipErrorInvalidValue;
     }
 }
@@ -649,8 +691,11 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
 
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {
     if (r.n_chunks > 0 && !r.chunks_are_tiles) {
-        k_reduce_chunks<<<dim3((unsigned)r.n_chunks), dim3(kBlock), 0, st>>>(r);
-        const hipError_t e = hipGetLastError();
+        const hipError_t e = in_pieces(r.n_chunks, kBlock, [&](int64_t b0, unsigned nb) {
+            ReduceParams q = r;
+            q.block0 = (int32_t)b0;
+            k_reduce_chunks<<<dim3(nb), dim3(kBlock), 0, st>>>(q);
+        });
         if (e != hipSuccess) return e;
     }
     k_reduce_finish<<<dim3(1), dim3(kFinishThreads), 0, st>>>(r);
@@ -661,23 +706,28 @@ hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, do
                                hipStream_t st) {
     if (P <= 0) return hipSuccess;
     const double llo = std::log(h_lo), lhi = std::log(h_hi);
-    k_init_problem<<<dim3(blocks_for((P + 3) / 4)), dim3(kBlock), 0, st>>>(
-        h, xs, P, round_keys(seed), (float)llo, (float)(lhi - llo));
-    return hipGetLastError();
+    const RoundKeys rk = round_keys(seed);
+    return groups_in_pieces((P + 3) / 4, [&](int64_t g0, int64_t, unsigned nb) {
+        k_init_problem<<<dim3(nb), dim3(kBlock), 0, st>>>(h, xs, P, rk, (float)llo, (float)(lhi - llo), g0);
+    });
 }
 
 hipError_t launch_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0, int64_t n,
                               uint32_t *out, hipStream_t st) {
     if (n <= 0) return hipSuccess;
-    k_philox_dump<<<dim3(blocks_for(n)), dim3(kBlock), 0, st>>>(round_keys(seed), c1, c2, c3, g0, n, out);
-    return hipGetLastError();
+    const RoundKeys rk = round_keys(seed);
+    return groups_in_pieces(n, [&](int64_t j0, int64_t m, unsigned nb) {
+        k_philox_dump<<<dim3(nb), dim3(kBlock), 0, st>>>(rk, c1, c2, c3, g0 + j0, m, out + 4 * j0);
+    });
 }
 
 hipError_t launch_normal_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0, int64_t n,
                               float *out, hipStream_t st) {
     if (n <= 0) return hipSuccess;
-    k_normal_dump<<<dim3(blocks_for(n)), dim3(kBlock), 0, st>>>(round_keys(seed), c1, c2, c3, g0, n, out);
-    return hipGetLastError();
+    const RoundKeys rk = round_keys(seed);
+    return groups_in_pieces(n, [&](int64_t j0, int64_t m, unsigned nb) {
+        k_normal_dump<<<dim3(nb), dim3(kBlock), 0, st>>>(rk, c1, c2, c3, g0 + j0, m, out + 4 * j0);
+    });
 }
 
 }  // namespace adpsgd

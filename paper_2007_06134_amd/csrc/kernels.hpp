@@ -18,6 +18,9 @@ constexpr int32_t kFinishWindow = 2048;
 // partials are the chunk partials and the first reduction launch is skipped.
 constexpr int64_t kDirectMaxTiles = kFinishWindow;
 constexpr int32_t kSmallTensorChunks = 32;  // larger tensors are summed by a wave, not a thread
+// Work-items per launch at most; a grid beyond it is issued in pieces of whole
+// 8-block groups, so the blocks keep their XCD order across the pieces.
+constexpr int64_t kMaxLaunchItems = int64_t(1) << 31;
 
 // One sync tile: a contiguous element range inside one tensor.
 struct Tile {
@@ -46,6 +49,10 @@ struct StepParams {
     uint32_t t;        // step index (Philox counter word 2)
     float sigma, mu, wd, gamma;
     RoundKeys rk;
+    // First block of this launch: a dispatch counts its grid in 32-bit
+    // work-items, so larger grids go out as several launches (the launchers
+    // below set it; callers leave it 0).
+    int64_t block0;
 };
 
 struct SyncParams {
@@ -59,13 +66,24 @@ struct SyncParams {
     SchedRule rule;
 };
 
-// Block sizes of the local step (threads = groups per block), and its grid
-// size for n_groups groups, K workers and a block size.
+// Launch shapes of the local step: threads per block (= float4 groups per
+// block) and an LDS reservation per block.  The kernel uses no LDS; the
+// reservation only holds a CU to floor(160 KB / lds) resident blocks, and
+// fewer waves in flight can stream HBM slightly faster.  The grid size for
+// n_groups groups, K workers and a block size is local_step_blocks.
+struct StepShape {
+    int block;
+    int lds;
+};
 constexpr int kStepBlocks[] = {64, 128, 256};
+constexpr int kMaxStepLds = 64 * 1024;
+// The shapes adpsgd_init times: the three block sizes, and 64-thread blocks
+// held to 20 per CU (8 KB each).
+constexpr StepShape kStepShapes[] = {{64, 0}, {64, 8192}, {128, 0}, {256, 0}};
 int64_t local_step_blocks(int64_t n_groups, int32_t K, int block);
 // vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4;
-// block: one of kStepBlocks (hipErrorInvalidValue otherwise).
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, int block, hipStream_t st);
+// block: one of kStepBlocks, lds in [0, kMaxStepLds] (hipErrorInvalidValue otherwise).
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, int block, int lds, hipStream_t st);
 // What a sync-tile kernel does:
 //   kAverage      average only (a separate sync);
 //   kFused        one local step, then average (a period's last step);
@@ -105,7 +123,7 @@ struct ReduceParams {
     const int32_t *large;         // [n_large] tensors of more than kSmallTensorChunks chunks
     int32_t n_chunks, T, K, n_large;
     int32_t chunks_are_tiles;     // 1: chunk_partials is tile_partials (one tile per chunk)
-    int32_t pad_;
+    int32_t block0;               // first chunk of this launch of the chunk sums (set by launch_reduce)
     double *out;                  // [2T]: variance per tensor, then gradient norm^2 (may be mapped host memory)
     SlotHdr *hdr;                 // (may be mapped host memory)
     SchedState *sched;            // non-null: the step's sync is decided and controlled here

@@ -192,8 +192,8 @@ struct adpsgd_ctx {
     bool vec = true;                // P % 4 == 0: dwordx4 rows
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
-    int32_t step_block = 256;       // block size of the plain local step in use
-    int32_t tuned_block = 256;      // the fastest one measured at init
+    StepShape step_shape{256, 0};   // launch shape of the plain local step in use
+    StepShape tuned_shape{256, 0};  // the fastest one measured at init
     RoundKeys rk{};
     bool timing = false;
     int32_t timing_every = 1;       // time every n-th launch of each class
@@ -311,13 +311,14 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
     p.wd = (float)c->hp.weight_decay;
     p.gamma = (float)adpsgd_lr(&c->hp, t);
     p.rk = c->rk;
+    p.block0 = 0;
     return p;
 }
 
 int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
     for (int64_t j = 0; j < n; ++j) {
         const StepParams p = step_params(c, t0 + j);
-        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->step_block, c->stream); });
+        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->step_shape.block, c->step_shape.lds, c->stream); });
         if (rc) return rc;
     }
     return ok();
@@ -356,7 +357,7 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     r.chunk_begin = c->d_chunk_begin;
     r.chunk_partials = c->chunks_are_tiles ? c->d_tile_partials : c->d_chunk_partials;
     r.chunks_are_tiles = c->chunks_are_tiles ? 1 : 0;
-    r.pad_ = 0;
+    r.block0 = 0;
     r.acc = c->d_acc;
     r.n_chunks = (int32_t)c->chunks.size();
     r.T = c->T;
@@ -402,23 +403,26 @@ struct Range {
     Range &operator=(const Range &) = delete;
 };
 
-// Time the local step at every block size on the context's own buffers (the
+// Time the local step in every launch shape on the context's own buffers (the
 // launches step x and m, which the caller zeroes afterwards): one warm-up
-// launch each, then three interleaved rounds; the fastest minimum wins.
-hipError_t tune_step_block(adpsgd_ctx *c) {
+// launch each, then five interleaved rounds; the fastest minimum wins.
+hipError_t tune_step_shape(adpsgd_ctx *c) {
     const StepParams p = step_params(c, 0);
-    constexpr int n = (int)(sizeof(kStepBlocks) / sizeof(kStepBlocks[0]));
+    constexpr int n = (int)(sizeof(kStepShapes) / sizeof(kStepShapes[0]));
     hipEvent_t a = nullptr, b = nullptr;
     hipError_t e = hipEventCreate(&a);
     if (e == hipSuccess) e = hipEventCreate(&b);
     float best[n];
     for (int j = 0; j < n; ++j) best[j] = 3.4e38f;
-    for (int j = 0; j < n && e == hipSuccess; ++j) e = launch_local_step(p, c->vec, c->nontemporal, kStepBlocks[j], c->stream);
-    for (int round = 0; round < 3 && e == hipSuccess; ++round) {
+    auto launch = [&](int j) {
+        return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j].block, kStepShapes[j].lds, c->stream);
+    };
+    for (int j = 0; j < n && e == hipSuccess; ++j) e = launch(j);
+    for (int round = 0; round < 5 && e == hipSuccess; ++round) {
         for (int j = 0; j < n && e == hipSuccess; ++j) {
             float ms = 0.f;
             if ((e = hipEventRecord(a, c->stream)) != hipSuccess) break;
-            if ((e = launch_local_step(p, c->vec, c->nontemporal, kStepBlocks[j], c->stream)) != hipSuccess) break;
+            if ((e = launch(j)) != hipSuccess) break;
             if ((e = hipEventRecord(b, c->stream)) != hipSuccess) break;
             if ((e = hipEventSynchronize(b)) != hipSuccess) break;
             if ((e = hipEventElapsedTime(&ms, a, b)) != hipSuccess) break;
@@ -429,7 +433,7 @@ hipError_t tune_step_block(adpsgd_ctx *c) {
         int win = n - 1;
         for (int j = 0; j < n; ++j)
             if (best[j] < best[win]) win = j;
-        c->tuned_block = c->step_block = kStepBlocks[win];
+        c->tuned_shape = c->step_shape = kStepShapes[win];
     }
     if (a) (void)hipEventDestroy(a);
     if (b) (void)hipEventDestroy(b);
@@ -460,8 +464,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if (!aligned(buf->x, 16) || !aligned(buf->m, 16) || !aligned(buf->h, 16) || !aligned(buf->xstar, 16))
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be 16-byte aligned");
     const Plan plan = count_plan(T, offsets);
-    if (plan.n_tiles >= (int64_t(1) << 31) || local_step_blocks((P + 3) / 4, K, kStepBlocks[0]) >= (int64_t(1) << 31))
-        return fail(ADPSGD_EINVAL, "K * P too large for one launch");
+    // tile indices are 32-bit in the chunk table (P / 4 < 2^32 keeps them far below)
+    if (plan.n_tiles >= (int64_t(1) << 31)) return fail(ADPSGD_EINVAL, "too many sync tiles");
     const Layout lay = layout_for(plan, T);
     if (!buf->workspace || !aligned(buf->workspace, 256)) return fail(ADPSGD_EINVAL, "workspace must be 256-byte aligned");
     if (buf->workspace_bytes < lay.total)
@@ -536,7 +540,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
         if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
         if ((double)K * (double)P >= kTuneMinElems) {
-            if ((e = tune_step_block(c)) != hipSuccess) return bail(e, "time the local step");
+            if ((e = tune_step_shape(c)) != hipSuccess) return bail(e, "time the local step");
             if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
             if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
         }
@@ -821,20 +825,25 @@ extern "C" int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in) {
     return ok();
 }
 
-extern "C" int adpsgd_set_step_block(adpsgd_ctx *c, int32_t block) {
+extern "C" int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes) {
     if (int rc = check_ctx(c)) return rc;
-    if (block == 0) block = c->tuned_block;
+    if (block == 0) {
+        c->step_shape = c->tuned_shape;
+        return ok();
+    }
     bool known = false;
     for (int b : kStepBlocks) known = known || b == block;
     if (!known) return fail(ADPSGD_EINVAL, "block must be 0, 64, 128 or 256");
-    c->step_block = block;
+    if (lds_bytes < 0 || lds_bytes > kMaxStepLds) return fail(ADPSGD_EINVAL, "lds_bytes must be in [0, 65536]");
+    c->step_shape = StepShape{block, lds_bytes};
     return ok();
 }
 
-extern "C" int adpsgd_get_step_block(const adpsgd_ctx *c, int32_t *block) {
+extern "C" int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes) {
     if (int rc = check_ctx(c)) return rc;
-    if (!block) return fail(ADPSGD_EINVAL, "block is NULL");
-    *block = c->step_block;
+    if (!block || !lds_bytes) return fail(ADPSGD_EINVAL, "block or lds_bytes is NULL");
+    *block = c->step_shape.block;
+    *lds_bytes = c->step_shape.lds;
     return ok();
 }
 

@@ -216,3 +216,95 @@ def test_full_size_adaptive_run_matches_oracle(A, key):
     _say(f"  {n} syncs identical; err x {ex:.2e} m {em:.2e} S {rel_err(recs['S'], g['S']):.2e}")
     assert ex < PARAM_TOL and em < MOM_TOL
     assert st.p == int(g["state_p"]) and st.nC2 == int(g["state_nC2"])
+
+
+def _torch_variance(torch, x, offsets, chunk=1 << 25):
+    """Per-tensor (1/K) sum_k sum_i (xbar_i - x_ki)^2 of the replicas in x [K, P],
+    in fp64 on the device, chunk by chunk (an independent check at any size)."""
+    K = x.shape[0]
+    out = np.zeros(len(offsets) - 1)
+    for tau in range(len(offsets) - 1):
+        acc = 0.0
+        for a in range(int(offsets[tau]), int(offsets[tau + 1]), chunk):
+            b = min(a + chunk, int(offsets[tau + 1]))
+            xc = x[:, a:b].double()
+            acc += float(((xc - xc.mean(dim=0)) ** 2).sum())
+            del xc
+        out[tau] = acc / K
+    return out
+
+
+def test_largest_problem_in_hbm(A):
+    """A problem sized to most of the GPU's memory (about 3.4e9 parameters of 8
+    workers on a 288 GB MI355X): every grid is larger than one dispatch can
+    hold, so the step and sync kernels run in several launches.  Checks the
+    oracle at sampled elements (whole small tensors, the elements around every
+    multiple of 2^28, where the launch pieces meet), the separate sync's
+    variance of every tensor against an fp64 recomputation on the device, and
+    that a fused sync leaves every replica equal."""
+    import torch
+    torch.cuda.empty_cache()
+    free, _ = torch.cuda.mem_get_info()
+    K = 8
+    P = int(0.75 * free / (8 * K + 8.5)) // 4 * 4
+    if K * P // 4 < 2 * (1 << 31):
+        pytest.skip(f"{free / 2**30:.0f} GiB free: too little memory for a multi-launch grid")
+    small = (1000, 7, 4093, 30001)
+    big1 = P // 2 + 12345
+    big2 = P - big1 - sum(small)
+    sizes = (small[0], small[1], big1, small[2], big2, small[3])
+    w = W.Workload(name=f"largest_k{K}", K=K, sizes=sizes, seed=11, sigma=0.02, momentum=0.9,
+                   weight_decay=5e-4, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.01, total_steps=8,
+                   period_mode=W.PERIOD_CONST, p_init=3, k_s=0)
+    off = w.offsets()
+    assert w.P == P
+    _say(f"largest problem: K={K} P={P} ({8 * K * P / 2**30:.0f} GiB of x and m, "
+         f"{free / 2**30:.0f} GiB free)")
+    rng = np.random.default_rng(5)
+    idx = [np.arange(off[0], off[2]), np.arange(off[3], off[4]), np.arange(off[5], off[6])]
+    for b in range(1 << 28, P, 1 << 28):
+        idx.append(np.arange(b - 300, min(b + 300, P)))
+    idx.append(rng.integers(0, P, size=4000))
+    idx = np.unique(np.concatenate(idx)).astype(np.int64)
+    whole = [0, 1, 3, 5]
+    it = torch.from_numpy(idx).cuda()
+
+    eng = A.Adpsgd.from_workload(w)
+    try:
+        eng.local_steps(2)                                   # steps 0, 1
+        torch.cuda.synchronize()
+        _say("  two steps done; fp64 variance on the device")
+        var_ref = _torch_variance(torch, eng.x, off)
+        var1 = eng.average()                                 # separate sync after step 1
+        _say("  separate sync done")
+        var2 = eng.step_average()                            # step 2 fused with its sync
+        torch.cuda.synchronize()
+        for a in range(0, P, 1 << 26):                       # every replica equals the mean
+            b = min(a + (1 << 26), P)
+            assert bool((eng.x[:, a:b] == eng.x[0:1, a:b]).all()), f"replicas differ in [{a}, {b})"
+        eng.local_steps(1)                                   # step 3
+        xs_sel = eng.x.index_select(1, it).double().cpu().numpy()
+        ms_sel = eng.m.index_select(1, it).double().cpu().numpy()
+    finally:
+        eng.close()
+        del eng
+        torch.cuda.empty_cache()
+    _say("  GPU part done; oracle replay of the sampled elements")
+    assert rel_err(var1, var_ref) < 1e-6
+
+    o = oracle.Oracle(w)
+    h, xs = o.problem_data(idx)
+    x = np.zeros((K, len(idx)))
+    v = np.zeros((K, len(idx)))
+    o.local_step(0, x, v, h, xs, idx)
+    o.local_step(1, x, v, h, xs, idx)
+    _, ov1 = o.average(x, idx)
+    o.local_step(2, x, v, h, xs, idx)
+    _, ov2 = o.average(x, idx)
+    o.local_step(3, x, v, h, xs, idx)
+    sub_off = np.searchsorted(idx, off)
+    assert max_rel_err(xs_sel, x, sub_off) < PARAM_TOL
+    assert max_rel_err(ms_sel, v, sub_off, floor=MOM_FLOOR) < MOM_TOL
+    for tau in whole:
+        assert rel_err(var1[tau], ov1[tau]) < VAR_TOL, tau
+        assert rel_err(var2[tau], ov2[tau]) < VAR_TOL, tau

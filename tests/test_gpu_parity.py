@@ -268,26 +268,35 @@ def test_manual_algorithm2_loop_equals_run(A, key, fused):
     assert st.C2 == pytest.approx(g["state"].C2, rel=1e-12)
 
 
-def test_step_block_sizes_agree_bitwise(A):
-    """The plain local step at every block size (the init-time choice among
+STEP_SHAPES = [(64, 0), (64, 8192), (128, 0), (256, 0), (256, 65536)]
+
+
+def test_step_launch_shapes_agree_bitwise(A):
+    """The plain local step in every launch shape (the init-time choice among
     them depends on timing) computes the same bits."""
     w = W.parity_workloads()["resnet18_like"].replace(total_steps=200, k_s=50)
     runs = {}
-    for bs in (64, 128, 256):
+    for shape in STEP_SHAPES:
         with A.Adpsgd.from_workload(w) as eng:
-            eng.set_step_block(bs)
-            assert eng.step_block == bs
+            eng.set_step_launch(*shape)
+            assert eng.step_launch == shape
             recs, var, n = eng.run(w.total_steps)
-            runs[bs] = (recs.tobytes(), var.tobytes(), eng.x.cpu().numpy().tobytes(), eng.m.cpu().numpy().tobytes())
+            runs[shape] = (recs.tobytes(), var.tobytes(), eng.x.cpu().numpy().tobytes(),
+                           eng.m.cpu().numpy().tobytes())
         with pytest.raises(A.AdpsgdError):
-            A.adpsgd_set_step_block(0, bs)   # a NULL context is refused
-    assert runs[64] == runs[128] == runs[256]
+            A.adpsgd_set_step_launch(0, *shape)   # a NULL context is refused
+    assert all(runs[s] == runs[STEP_SHAPES[0]] for s in STEP_SHAPES)
     with A.Adpsgd.from_workload(w) as eng:
-        with pytest.raises(A.AdpsgdError) as e:
-            eng.set_step_block(96)
-        assert e.value.code == A.EINVAL
-        eng.set_step_block(0)
-        assert eng.step_block in (64, 128, 256)
+        tuned = eng.step_launch
+        assert tuned in STEP_SHAPES[:4]
+        for bad in [(96, 0), (64, -1), (64, 65537)]:
+            with pytest.raises(A.AdpsgdError) as e:
+                eng.set_step_launch(*bad)
+            assert e.value.code == A.EINVAL
+            assert eng.step_launch == tuned
+        eng.set_step_launch(256, 4096)
+        eng.set_step_launch(0, 123)                # back to the timed choice
+        assert eng.step_launch == tuned
 
 
 def _random_workload(i):
