@@ -25,15 +25,15 @@ def lib_path() -> str:
     return _LIB
 
 
-def build_oracle() -> str:
+def build_oracle(src: str = _SRC, out: str = _LIB) -> str:
     """Compile the oracle with plain IEEE fp64 (no fast-math, no FMA contraction)."""
-    tmp = _LIB + f".tmp{os.getpid()}"
+    tmp = out + f".tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
            "-fno-fast-math", "-ffp-contract=off", "-Wall", "-Wextra",
-           _SRC, "-o", tmp, "-lm"]
+           src, "-o", tmp, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB)
-    return _LIB
+    os.replace(tmp, out)
+    return out
 
 
 class _Problem(C.Structure):
@@ -67,13 +67,19 @@ _U32 = C.POINTER(C.c_uint32)
 
 
 def _load():
+    """The compiled oracle; ADPSGD_ORACLE_LIB names another build of the same
+    source to load instead (the mutation test points the pins at copies with a
+    planted mistake)."""
     global _lib
     with _lock:
         if _lib is not None:
             return _lib
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build_oracle()
-        lib = C.CDLL(_LIB)
+        path = os.environ.get("ADPSGD_ORACLE_LIB")
+        if not path:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build_oracle()
+        lib = C.CDLL(path)
         lib.orc_philox4x32_10.argtypes = [_U32, _U32, _U32]
         lib.orc_normals4.argtypes = [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32, _D]
         lib.orc_lr.argtypes = [C.POINTER(_Problem), C.c_int64]
