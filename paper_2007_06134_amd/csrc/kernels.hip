@@ -179,6 +179,19 @@ __device__ __forceinline__ f4 tree_sum_lds(const f4 (*rows)[64], int lane, int b
     }
 }
 
+// The same tree over a thread's own registers v[base .. base+N).  For N and K
+// powers of two, rows R w .. R w + R - 1 form one node of the K-row tree, so
+// summing a wave's R rows here and the W node sums through LDS gives the same
+// bits as the K-row tree.
+template <int N>
+__device__ __forceinline__ f4 tree_sum_regs(const f4 *v, int base) {
+    if constexpr (N == 1) {
+        return v[base];
+    } else {
+        return tree_sum_regs<N / 2>(v, base) + tree_sum_regs<N - N / 2>(v, base + N / 2);
+    }
+}
+
 // Step s.t of a run whose schedule lives on the device: does a sync follow
 // it?  Every thread reads the same state (written only by the reduction
 // kernel after a sync), so the answer is uniform over the launch.
@@ -189,11 +202,12 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 }
 
 // One tile (at most 64 groups, one per lane) of one tensor.  Wave w owns the
-// rows k = w, w + W, ... (W waves, R = K / W rows each; see sync_waves).  Each
-// thread steps its rows (modes with a step), publishes them in LDS, reads all
-// K rows of its lane back to form the mean in a fixed order (the same bits in
-// every thread), sums its squared deviations and, when a sync is due, writes
-// the mean over its rows (with averaged momentum, the momentum rows too).  The
+// rows k = R w .. R w + R - 1 (W waves, R = K / W rows each; see sync_waves).
+// Each thread steps its rows (modes with a step), publishes their pairwise sum
+// in LDS, reads the W sums of its lane back to form the mean in a fixed order
+// (the same bits in every thread, and the same as a tree over all K rows),
+// sums its squared deviations and, when a sync is due, writes the mean over
+// its rows (with averaged momentum, the momentum rows too).  The
 // traced mode also sums the squared gradient norm at the mean (wave 0 counts
 // each element once).  partials[2 tile + {0, 1}] = (sum of squared
 // deviations, gradient norm^2).  In kDevice a step without a sync stores the
@@ -213,8 +227,9 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     constexpr int R = KT / W;
     constexpr bool STEP = MODE != kAverage;
     constexpr bool GN = MODE == kDeviceTrace;
-    __shared__ f4 rows[KT][64];
-    __shared__ f4 mrows[AVGM ? KT : 1][64];
+    // wave w owns rows R w .. R w + R - 1 and publishes their subtree sum
+    __shared__ f4 part[W][64];
+    __shared__ f4 mpart[AVGM ? W : 1][64];
     const StepParams &a = p.s;
     bool bcast = true;  // the host-decided modes always average
     if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
@@ -234,10 +249,10 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         f4 m[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
+            float *xrow = a.x + (int64_t)(R * w + r) * a.P + e0;
             xr[r] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
             if (STEP || AVGM) {
-                float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
+                float *mrow = a.m + (int64_t)(R * w + r) * a.P + e0;
                 m[r] = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
             }
         }
@@ -248,7 +263,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         if (STEP) {
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                const int k = w + W * r;
+                const int k = R * w + r;
                 sgd_update(a, xr[r], m[r], h, xs, step_noise(a, g, k));
                 if (!avg_m) {
                     float *mrow = a.m + (int64_t)k * a.P + e0;
@@ -261,18 +276,15 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (measure) {
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                rows[w + W * r][lane] = xr[r];
-                if (AVGM) mrows[w + W * r][lane] = m[r];
-            }
+            part[w][lane] = tree_sum_regs<R>(xr, 0);
+            if (AVGM) mpart[w][lane] = tree_sum_regs<R>(m, 0);
         }
     }
     if (!measure) return;  // uniform over the block
     __syncthreads();
     double acc = 0.0, gn = 0.0;
     if (active) {
-        const f4 mean = tree_sum_lds<KT>(rows, lane, 0) / splat((float)KT);
+        const f4 mean = tree_sum_lds<W>(part, lane, 0) / splat((float)KT);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             // squared deviations in fp32 per element, each row's sum in fp64
@@ -281,15 +293,15 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             if (!full) d2 = mask4(d2, e0, lo, hi);
             acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
             if (bcast) {
-                float *xrow = a.x + (int64_t)(w + W * r) * a.P + e0;
+                float *xrow = a.x + (int64_t)(R * w + r) * a.P + e0;
                 if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
             }
         }
         if (avg_m) {
-            const f4 mmean = tree_sum_lds<KT>(mrows, lane, 0) / splat((float)KT);
+            const f4 mmean = tree_sum_lds<W>(mpart, lane, 0) / splat((float)KT);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                float *mrow = a.m + (int64_t)(w + W * r) * a.P + e0;
+                float *mrow = a.m + (int64_t)(R * w + r) * a.P + e0;
                 if (full) st4<NT>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
             }
         }

@@ -16,6 +16,8 @@ constexpr int32_t kChunkTiles = 1024;  // tiles per first-level chunk of the var
 constexpr int32_t kFinishWindow = 2048;
 // Up to this many tiles (one LDS window), every tile is its own chunk: the tile
 // partials are the chunk partials and the first reduction launch is skipped.
+// (Above it, the one finishing block reading every tile partial costs more
+// than the chunk launch: 22 us against 9 us for the pair at 5080 tiles.)
 constexpr int64_t kDirectMaxTiles = kFinishWindow;
 constexpr int32_t kSmallTensorChunks = 32;  // larger tensors are summed by a wave, not a thread
 // Work-items per launch at most; a grid beyond it is issued in pieces of whole

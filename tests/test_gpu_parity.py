@@ -189,6 +189,47 @@ def test_run_matches_oracle(A, key):
         assert rel_err([g["state"].C2], [r.state.C2]) < VAR_TOL
 
 
+def _sizes_with_tiles(n_tiles, seed, max_size):
+    """Ragged tensor sizes (log-uniform in [1, max_size]) whose sync tiles (cut
+    at multiples of 256 elements, never across a tensor) number exactly n_tiles."""
+    rng = np.random.default_rng(seed)
+    sizes, start, tiles = [], 0, 0
+    while tiles < n_tiles:
+        size = int(np.exp(rng.uniform(0.0, np.log(max_size))))
+        t = (start + size + 255) // 256 - start // 256
+        if tiles + t >= n_tiles:      # last tensor: end inside the tile that completes the count
+            end = (start // 256 + n_tiles - tiles - 1) * 256 + 1 + int(rng.integers(0, 255))
+            size = end - start
+            t = n_tiles - tiles
+        sizes.append(size)
+        start += size
+        tiles += t
+    return tuple(sizes)
+
+
+@pytest.mark.parametrize("n_tiles,max_size", [(2048, 60_000), (2049, 60_000), (8300, 60_000), (4500, 400)])
+def test_reduction_paths_match_oracle(A, n_tiles, max_size):
+    """Tile counts on either side of each change of the variance reduction's
+    path: every tile its own chunk (up to 2048 tiles, one launch), then chunks
+    of tiles summed first (two launches); with thousands of small tensors the
+    chunk partials outgrow the finishing block's LDS window and pass through it
+    in several windows."""
+    sizes = _sizes_with_tiles(n_tiles, n_tiles, max_size)
+    w = W.Workload(name=f"tiles_{n_tiles}", K=4, sizes=sizes, seed=n_tiles, sigma=0.1, momentum=0.9,
+                   weight_decay=5e-4, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.05,
+                   total_steps=16, period_mode=W.PERIOD_ADAPTIVE, p_init=2, k_s=6)
+    _say(f"reduction paths: {n_tiles} tiles, T={w.T}, P={w.P}")
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    recs = g["recs"]
+    assert np.array_equal(recs["t"], r.sync_t) and np.array_equal(recs["p"], r.sync_p)
+    assert rel_err(recs["S"], r.S) < VAR_TOL
+    assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
+    off = w.offsets()
+    assert max_rel_err(g["x"], r.x, off) < PARAM_TOL
+    assert max_rel_err(g["m"], r.v, off, floor=MOM_FLOOR) < MOM_TOL
+
+
 def test_period_one_replicas_stay_identical(A):
     w = _tiny(K=8, sizes=(6000, 2001), p_init=1, total_steps=12)
     with A.Adpsgd.from_workload(w) as eng:
