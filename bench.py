@@ -122,7 +122,7 @@ def main():
                     help="only run a plain device copy of MIB MiB (x3), to scale byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only (the K workers share one GPU's HBM); "
+        print("bench.py: the K workers share one GPU's HBM, so the library runs on one GPU; "
               "--gpus must be 1", file=sys.stderr)
         sys.exit(2)
 
