@@ -185,7 +185,7 @@ def test_full_size_launch_policies_agree(A):
         assert torch.equal(o[2], base[2]) and torch.equal(o[3], base[3]), pol
 
 
-@pytest.mark.parametrize("key", ["resnet18_like", "many_small"])
+@pytest.mark.parametrize("key", ["resnet18_like", "resnet50_like", "vgg16_adaptive", "many_small"])
 def test_full_size_adaptive_run_matches_oracle(A, key):
     """The whole adaptive run at full size, in the bench's launch configuration,
     against the oracle's own full run (tests/golden/fullsize_<key>.npz, written
