@@ -3,7 +3,8 @@
 Argument marshalling only: every step of the hot path runs in the library's
 HIP kernels.  Functions keep the C names; a failing status raises
 ``AdpsgdError`` carrying the library's message.  If the library has not been
-built, importing this module raises ImportError (there is no fallback).
+built, importing this module builds it (hipcc, gfx950); if that fails it
+raises ImportError (there is no fallback).
 """
 from __future__ import annotations
 
@@ -71,7 +72,14 @@ class adpsgd_timing(C.Structure):
 
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2007_06134_amd.build`")
+    # nothing built yet: build it now with hipcc (gfx950); if that fails there is
+    # no library and no fallback
+    try:
+        from . import build as _build
+        _build.build()
+    except Exception as e:  # noqa: BLE001
+        raise ImportError(f"{LIB_PATH} is not built and building it failed ({e}); "
+                          "run `python -m paper_2007_06134_amd.build`") from e
 
 lib = C.CDLL(LIB_PATH)
 
