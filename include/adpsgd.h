@@ -20,6 +20,8 @@
  *   - Device buffers are caller-owned (the library never allocates or frees
  *     them).  Host arrays are read during the call and never retained, except
  *     where stated.
+ *   - Calls on a context make its device (the one current at adpsgd_init)
+ *     current while they run and restore the caller's device afterwards.
  *   - One context is used by one host thread at a time.  A context pointer that
  *     adpsgd_init did not return, or that was destroyed, is refused with
  *     ADPSGD_EINVAL (so is a second adpsgd_destroy).

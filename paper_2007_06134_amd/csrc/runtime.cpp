@@ -395,6 +395,22 @@ int check_ctx(const adpsgd_ctx *c) {
     return ok();
 }
 
+// The context's device made current for the duration of a call, and the
+// caller's restored afterwards (a context's buffers, stream and events belong
+// to the device that was current at adpsgd_init).
+struct DeviceScope {
+    int prev = -1;
+    explicit DeviceScope(const adpsgd_ctx *c) {
+        int cur = -1;
+        if (hipGetDevice(&cur) == hipSuccess && cur != c->device && hipSetDevice(c->device) == hipSuccess) prev = cur;
+    }
+    ~DeviceScope() {
+        if (prev >= 0) (void)hipSetDevice(prev);
+    }
+    DeviceScope(const DeviceScope &) = delete;
+    DeviceScope &operator=(const DeviceScope &) = delete;
+};
+
 // A roctx range for the duration of a call (visible with rocprofv3 --marker-trace).
 struct Range {
     explicit Range(const char *name) { roctxRangePushA(name); }
@@ -558,6 +574,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
 
 extern "C" int adpsgd_reset(adpsgd_ctx *c) {
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (c->P > 0) {
         const size_t bytes = sizeof(float) * (size_t)c->K * (size_t)c->P;
         HIP_TRY(hipMemsetAsync(c->buf.x, 0, bytes, c->stream));
@@ -571,6 +588,7 @@ extern "C" int adpsgd_reset(adpsgd_ctx *c) {
 extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
     Range range_("adpsgd_local_steps");
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (n < 0) return fail(ADPSGD_EINVAL, "n must be >= 0");
     if (c->st.t + n > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
     if (int rc = enqueue_steps(c, c->st.t, n)) return rc;
@@ -582,6 +600,7 @@ extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
 static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
     Range range_("adpsgd_sync");
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (!var_out) return fail(ADPSGD_EINVAL, "var_out is NULL");
     if (fused && c->st.t + 1 > kMaxCounter) return fail(ADPSGD_EINVAL, "step index would reach 2^32");
     if (int rc = enqueue_sync(c, fused ? kFused : kAverage, c->st.t, 0, false, nullptr)) return rc;
@@ -623,6 +642,7 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
                     adpsgd_step_rec *trace, int64_t trace_cap, int64_t *n_syncs) {
     Range range_("adpsgd_run");
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (n_steps < 0 || log_cap < 0 || trace_cap < 0) return fail(ADPSGD_EINVAL, "n_steps and capacities must be >= 0");
     if (log_cap > 0 && !log) return fail(ADPSGD_EINVAL, "log is NULL with log_cap > 0");
     if (trace_cap > 0 && !trace) return fail(ADPSGD_EINVAL, "trace is NULL with trace_cap > 0");
@@ -857,6 +877,7 @@ extern "C" int adpsgd_set_launch_policy(adpsgd_ctx *c, int32_t policy) {
 
 extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t every) {
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (every < 0) return fail(ADPSGD_EINVAL, "every must be >= 0");
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (int rc = harvest(c, true)) return rc;
@@ -869,6 +890,7 @@ extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t every) {
 
 extern "C" int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out) {
     if (int rc = check_ctx(c)) return rc;
+    DeviceScope dev_(c);
     if (!out) return fail(ADPSGD_EINVAL, "out is NULL");
     HIP_TRY(hipStreamSynchronize(c->stream));
     if (int rc = harvest(c, true)) return rc;
@@ -884,8 +906,12 @@ extern "C" int adpsgd_destroy(adpsgd_ctx *c) {
         std::lock_guard<std::mutex> lock(g_live_mu);
         if (!g_live.erase(c)) return fail(ADPSGD_EINVAL, "not a live context (destroyed twice?)");
     }
-    hipError_t e = hipStreamSynchronize(c->stream);
-    release(c);
+    hipError_t e;
+    {
+        DeviceScope dev_(c);
+        e = hipStreamSynchronize(c->stream);
+        release(c);
+    }
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     return ok();
 }
