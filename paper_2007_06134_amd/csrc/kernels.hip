@@ -607,30 +607,53 @@ hipError_t groups_in_pieces(int64_t n, F launch) {
     return hipSuccess;
 }
 
-template <int KT, int MODE, bool AVGM>
-hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, hipStream_t st) {
+// Dynamic LDS that holds a CU to `cap` resident blocks of a kernel with
+// static_lds bytes of its own: each block then takes kLdsPerCU / cap bytes
+// (rounded down to 512).  0 for no cap, or when the kernel's own LDS already
+// allows no more.
+inline int cap_lds(int cap, size_t static_lds) {
+    if (cap <= 0) return 0;
+    const size_t per_block = (size_t)(kLdsPerCU / cap) & ~size_t(511);
+    return per_block > static_lds ? (int)(per_block - static_lds) : 0;
+}
+
+template <class Kern>
+size_t static_lds_of(Kern kern) {
+    hipFuncAttributes fa;
+    return hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kern)) == hipSuccess ? fa.sharedSizeBytes : 0;
+}
+
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
+hipError_t sync_variant(const SyncParams &p, int64_t n_tiles, int cap, hipStream_t st) {
     constexpr int threads = 64 * sync_waves<KT, MODE>();
+    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM>);
+    const int lds = cap_lds(cap, own);
     return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
         SyncParams q = p;
         q.s.block0 = b0;
-        if (vec && nt) k_sync_lds<KT, true, true, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
-        else if (vec) k_sync_lds<KT, true, false, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
-        else k_sync_lds<KT, false, false, MODE, AVGM><<<dim3(nb), dim3(threads), 0, st>>>(q);
+        k_sync_lds<KT, VEC, NT, MODE, AVGM><<<dim3(nb), dim3(threads), lds, st>>>(q);
     });
 }
 
+template <int KT, int MODE, bool AVGM>
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, int cap, hipStream_t st) {
+    if (vec && nt) return sync_variant<KT, true, true, MODE, AVGM>(p, n_tiles, cap, st);
+    if (vec) return sync_variant<KT, true, false, MODE, AVGM>(p, n_tiles, cap, st);
+    return sync_variant<KT, false, false, MODE, AVGM>(p, n_tiles, cap, st);
+}
+
 template <int KT>
-hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,
+hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt, int cap,
                          hipStream_t st) {
     switch (mode) {
-    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true>(p, n_tiles, vec, nt, st)
-                                : sync_dispatch<KT, kAverage, false>(p, n_tiles, vec, nt, st);
-    case kFused: return avg_m ? sync_dispatch<KT, kFused, true>(p, n_tiles, vec, nt, st)
-                              : sync_dispatch<KT, kFused, false>(p, n_tiles, vec, nt, st);
-    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true>(p, n_tiles, vec, nt, st)
-                               : sync_dispatch<KT, kDevice, false>(p, n_tiles, vec, nt, st);
-    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true>(p, n_tiles, vec, nt, st)
-                          : sync_dispatch<KT, kDeviceTrace, false>(p, n_tiles, vec, nt, st);
+    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true>(p, n_tiles, vec, nt, cap, st)
+                                : sync_dispatch<KT, kAverage, false>(p, n_tiles, vec, nt, cap, st);
+    case kFused: return avg_m ? sync_dispatch<KT, kFused, true>(p, n_tiles, vec, nt, cap, st)
+                              : sync_dispatch<KT, kFused, false>(p, n_tiles, vec, nt, cap, st);
+    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true>(p, n_tiles, vec, nt, cap, st)
+                               : sync_dispatch<KT, kDevice, false>(p, n_tiles, vec, nt, cap, st);
+    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true>(p, n_tiles, vec, nt, cap, st)
+                          : sync_dispatch<KT, kDeviceTrace, false>(p, n_tiles, vec, nt, cap, st);
     }
 }
 
@@ -687,16 +710,29 @@ hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, int block, 
     }
 }
 
+int sync_tile_waves(int K, int mode) {
+    const bool avg = mode == kAverage;
+    switch (K) {
+    case 1: return avg ? sync_waves<1, kAverage>() : sync_waves<1, kFused>();
+    case 2: return avg ? sync_waves<2, kAverage>() : sync_waves<2, kFused>();
+    case 4: return avg ? sync_waves<4, kAverage>() : sync_waves<4, kFused>();
+    case 8: return avg ? sync_waves<8, kAverage>() : sync_waves<8, kFused>();
+    case 16: return avg ? sync_waves<16, kAverage>() : sync_waves<16, kFused>();
+    case 32: return avg ? sync_waves<32, kAverage>() : sync_waves<32, kFused>();
+    default: return 0;
+    }
+}
+
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt,
-                            hipStream_t st) {
+                            int cap, hipStream_t st) {
     if (n_tiles <= 0) return hipSuccess;
     switch (p.s.K) {
-    case 1: return sync_dispatch<1>(p, n_tiles, mode, avg_m, vec, nt, st);
-    case 2: return sync_dispatch<2>(p, n_tiles, mode, avg_m, vec, nt, st);
-    case 4: return sync_dispatch<4>(p, n_tiles, mode, avg_m, vec, nt, st);
-    case 8: return sync_dispatch<8>(p, n_tiles, mode, avg_m, vec, nt, st);
-    case 16: return sync_dispatch<16>(p, n_tiles, mode, avg_m, vec, nt, st);
-    case 32: return sync_dispatch<32>(p, n_tiles, mode, avg_m, vec, nt, st);
+    case 1: return sync_dispatch<1>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+    case 2: return sync_dispatch<2>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+    case 4: return sync_dispatch<4>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+    case 8: return sync_dispatch<8>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+    case 16: return sync_dispatch<16>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+    case 32: return sync_dispatch<32>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
     default: return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
     }
 }

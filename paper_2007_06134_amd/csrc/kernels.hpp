@@ -97,9 +97,17 @@ enum SyncMode : int { kAverage = 0, kFused = 1, kDevice = 2, kDeviceTrace = 3 };
 
 // Tile partials are pairs (sum of squared deviations, squared gradient norm at
 // the mean; the latter only when tracing).  avg_m = true: a sync also averages
-// the momentum buffers.
+// the momentum buffers.  cap > 0 reserves LDS (160 KB per CU on gfx950) so
+// that at most cap blocks of the sync-tile kernel are resident per CU; 0: none.
+// The loop kernel (K without a compiled variant) ignores it.
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec,
-                            bool nontemporal, hipStream_t st);
+                            bool nontemporal, int cap, hipStream_t st);
+// Waves per block of the sync-tile kernel for K workers in a mode (0 when K
+// takes the loop kernel).
+int sync_tile_waves(int K, int mode);
+constexpr int kLdsPerCU = 160 * 1024;
+// Resident waves per CU that the separate sync is timed with at init.
+constexpr int kAverageCapWaves = 24;
 
 // Record of one launch of the reduction kernel (one step or one sync).
 struct SlotHdr {

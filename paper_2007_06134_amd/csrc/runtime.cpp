@@ -194,6 +194,7 @@ struct adpsgd_ctx {
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
     StepShape step_shape{256, 0};   // launch shape of the plain local step in use
     StepShape tuned_shape{256, 0};  // the fastest one measured at init
+    int32_t average_cap = 0;        // resident blocks per CU of the separate sync (0: no cap), timed at init
     RoundKeys rk{};
     bool timing = false;
     int32_t timing_every = 1;       // time every n-th launch of each class
@@ -348,7 +349,10 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     const int kind = dev ? -1 : mode == kAverage ? tAverage : tFused;
     int rc = timed_launch(
         c, kind,
-        [&] { return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal, c->stream); },
+        [&] {
+            return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
+                                    mode == kAverage ? c->average_cap : 0, c->stream);
+        },
         step_seq);
     if (rc) return rc;
     ReduceParams r;
@@ -456,6 +460,42 @@ hipError_t tune_step_shape(adpsgd_ctx *c) {
     return e;
 }
 
+// Time the separate sync (mean, broadcast and variance of every tile, no step)
+// without and with an LDS cap that holds a CU to kAverageCapWaves resident
+// waves, on the context's own buffers (zeroed again afterwards); one warm-up
+// launch each, then five interleaved rounds; the fastest minimum wins.
+hipError_t tune_average_cap(adpsgd_ctx *c) {
+    const int waves = sync_tile_waves(c->K, kAverage);
+    if (waves <= 0 || c->tiles.empty()) return hipSuccess;
+    const int caps[2] = {0, std::max(1, kAverageCapWaves / waves)};
+    const SyncParams sp = sync_params(c, 0);
+    const int64_t n_tiles = (int64_t)c->tiles.size();
+    auto launch = [&](int j) {
+        return launch_tile_sync(sp, n_tiles, kAverage, c->hp.avg_momentum != 0, c->vec, c->nontemporal, caps[j],
+                                c->stream);
+    };
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    float best[2] = {3.4e38f, 3.4e38f};
+    for (int j = 0; j < 2 && e == hipSuccess; ++j) e = launch(j);
+    for (int round = 0; round < 5 && e == hipSuccess; ++round) {
+        for (int j = 0; j < 2 && e == hipSuccess; ++j) {
+            float ms = 0.f;
+            if ((e = hipEventRecord(a, c->stream)) != hipSuccess) break;
+            if ((e = launch(j)) != hipSuccess) break;
+            if ((e = hipEventRecord(b, c->stream)) != hipSuccess) break;
+            if ((e = hipEventSynchronize(b)) != hipSuccess) break;
+            if ((e = hipEventElapsedTime(&ms, a, b)) != hipSuccess) break;
+            best[j] = std::min(best[j], ms);
+        }
+    }
+    if (e == hipSuccess) c->average_cap = best[1] < best[0] ? caps[1] : 0;
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    return e;
+}
+
 }  // namespace
 
 extern "C" const char *adpsgd_last_error(void) { return g_last_error.c_str(); }
@@ -557,6 +597,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
         if ((double)K * (double)P >= kTuneMinElems) {
             if ((e = tune_step_shape(c)) != hipSuccess) return bail(e, "time the local step");
+            if ((e = tune_average_cap(c)) != hipSuccess) return bail(e, "time the separate sync");
             if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
             if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
         }
