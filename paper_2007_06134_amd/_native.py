@@ -81,6 +81,13 @@ if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built and building it failed ({e}); "
                           "run `python -m paper_2007_06134_amd.build`") from e
 
+# One HIP runtime per process.  torch ships its own libamdhip64 and finds it
+# next to its libraries; this library asks for libamdhip64.so.7, which the
+# loader resolves to whatever is already loaded under that name.  Importing
+# torch first makes that torch's copy.  Loaded the other way round, the
+# process would hold two runtimes and this library's would see no device.
+import torch  # noqa: E402,F401
+
 lib = C.CDLL(LIB_PATH)
 
 _CTX = C.c_void_p

@@ -365,11 +365,12 @@ def _random_workload(i):
     return W.Workload(**kw)
 
 
-@pytest.mark.parametrize("i", range(16))
+@pytest.mark.parametrize("i", range(128))
 def test_random_workloads_match_oracle(A, i):
-    """Sixteen seeded random configurations against the oracle (x, m, the sync
-    list, S and the per-tensor variances).  Every decision of these seeds lies
-    more than 5% from a threshold in the oracle, far above fp32 rounding."""
+    """128 seeded random configurations against the oracle (x, m, the sync
+    list, S and the per-tensor variances).  The closest decision of these seeds
+    lies 5e-4 from a threshold (seed 50, where S is within 2.4e-7 of the
+    oracle's); the others at least 1.7e-3."""
     w = _random_workload(i)
     _say(f"random {i}: K={w.K} P={w.P} T={w.T} mode={w.period_mode} N={w.total_steps}")
     g = gpu_run(w)
@@ -380,6 +381,32 @@ def test_random_workloads_match_oracle(A, i):
     assert max_rel_err(g["x"], r.x, w.offsets()) < PARAM_TOL
     assert max_rel_err(g["m"], r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
     assert g["state"].t == w.total_steps and g["state"].p == r.state.p
+
+
+def test_package_imported_before_torch(A):
+    """In a fresh process that imports this package before torch, the library
+    binds to the same HIP runtime as torch (one runtime per process) and a run
+    gives the same bits as here."""
+    import hashlib
+    import os
+    import subprocess
+    w = W.parity_workloads()["many_small"].replace(total_steps=40, k_s=10)
+    g = gpu_run(w)
+    want = hashlib.sha256(g["x"].tobytes() + g["m"].tobytes()).hexdigest()
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = (
+        "import sys, hashlib\n"
+        "import paper_2007_06134_amd\n"          # before torch, on purpose
+        "sys.path.insert(0, 'tests')\n"
+        "import workloads as W\n"
+        "from helpers import gpu_run\n"
+        "w = W.parity_workloads()['many_small'].replace(total_steps=40, k_s=10)\n"
+        "g = gpu_run(w)\n"
+        "print(hashlib.sha256(g['x'].tobytes() + g['m'].tobytes()).hexdigest())\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=240,
+                       env=dict(os.environ, PYTHONPATH=root))
+    assert r.returncode == 0, r.stderr[-3000:]
+    assert r.stdout.strip().splitlines()[-1] == want
 
 
 def test_checkpoint_resume_is_bit_exact(A):
