@@ -199,7 +199,9 @@ ADPSGD_API int adpsgd_reset(adpsgd_ctx *c);
 
 /* Enqueue n >= 0 plain local steps t .. t+n-1 on every worker (Algorithm 2,
  * lines 5-7): d = h (x - x*) + sigma z + wd x; m = mu m + d; x = x - gamma_t m.
- * Advances t and cnt by n.  Asynchronous. */
+ * Advances t and cnt by n; a constant period that switches at p_switch_step
+ * (hparams) becomes p_after in the state once a step t >= p_switch_step is
+ * taken, as in adpsgd_sched_step.  Asynchronous. */
 ADPSGD_API int adpsgd_local_steps(adpsgd_ctx *c, int32_t n);
 
 /* Synchronize now (Algorithm 2, lines 9-12): xbar = mean of the K replicas,
@@ -209,7 +211,8 @@ ADPSGD_API int adpsgd_local_steps(adpsgd_ctx *c, int32_t n);
 ADPSGD_API int adpsgd_average(adpsgd_ctx *c, double *var_out);
 
 /* One local step followed by the synchronization, in a single pass over x and
- * m (same results as adpsgd_local_steps(c, 1) then adpsgd_average).  Blocks. */
+ * m (same results and state as adpsgd_local_steps(c, 1) then adpsgd_average).
+ * Blocks. */
 ADPSGD_API int adpsgd_step_average(adpsgd_ctx *c, double *var_out);
 
 /* Period controller (Algorithm 2, lines 13-19) for a sync after step t - 1 with

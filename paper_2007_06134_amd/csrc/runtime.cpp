@@ -635,6 +635,8 @@ extern "C" int adpsgd_local_steps(adpsgd_ctx *c, int32_t n) {
     if (int rc = enqueue_steps(c, c->st.t, n)) return rc;
     c->st.t += n;
     c->st.cnt += n;
+    // a constant period that switches at p_switch_step does so for the state too
+    if (n > 0) c->st.p = period_at(rule_of(&c->hp), c->st.p, c->st.t - 1);
     return ok();
 }
 
@@ -647,7 +649,10 @@ static int sync_now(adpsgd_ctx *c, bool fused, double *var_out) {
     if (int rc = enqueue_sync(c, fused ? kFused : kAverage, c->st.t, 0, false, nullptr)) return rc;
     HIP_TRY(hipEventSynchronize(c->ring_ev[0]));
     std::memcpy(var_out, slot_host(c, 0) + kSlotHdrBytes, sizeof(double) * c->T);
-    if (fused) c->st.t += 1;
+    if (fused) {
+        c->st.p = period_at(rule_of(&c->hp), c->st.p, c->st.t);
+        c->st.t += 1;
+    }
     c->st.cnt = 0;
     return ok();
 }
