@@ -409,6 +409,46 @@ def test_package_imported_before_torch(A):
     assert r.stdout.strip().splitlines()[-1] == want
 
 
+def _run_digest(A, w, stream=None):
+    import hashlib
+    import torch
+    with A.Adpsgd.from_workload(w, stream=stream) as eng:
+        recs, var, _ = eng.run(w.total_steps)
+        eng.local_steps(3)
+        v2 = eng.average()
+        torch.cuda.synchronize()
+        blob = eng.x.cpu().numpy().tobytes() + eng.m.cpu().numpy().tobytes() + recs.tobytes()
+    return hashlib.sha256(blob + var.tobytes() + v2.tobytes()).hexdigest()
+
+
+def test_side_streams_and_concurrent_contexts_agree_bitwise(A):
+    """A context on a non-default stream (current, or passed while the default
+    one is current), and several contexts on their own streams driven from as
+    many host threads at once, give the bits of a default-stream run: all work
+    of a context is ordered on its stream."""
+    import threading
+    import torch
+    ws = [W.parity_workloads()[k].replace(total_steps=120, k_s=30)
+          for k in ("resnet18_like", "many_small", "vgg16_adaptive")]
+    base = [_run_digest(A, w) for w in ws]
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        assert [_run_digest(A, w, stream=side) for w in ws] == base
+    assert [_run_digest(A, w, stream=side) for w in ws] == base
+    for _ in range(2):
+        out = {}
+
+        def worker(j):
+            out[j] = _run_digest(A, ws[j], stream=torch.cuda.Stream())
+
+        threads = [threading.Thread(target=worker, args=(j,)) for j in range(len(ws))]
+        for th in threads:
+            th.start()
+        for th in threads:
+            th.join()
+        assert [out.get(j) for j in range(len(ws))] == base
+
+
 def test_checkpoint_resume_is_bit_exact(A):
     import torch
     w = W.parity_workloads()["resnet18_like"].replace(total_steps=700, k_s=150)
