@@ -165,6 +165,7 @@ def main():
     elapsed = time.perf_counter() - t0
     tm = eng.get_timing()
     step_block, step_lds = eng.step_launch
+    row_stride = eng.row_stride
     sep = None
     if not args.no_timing:
         # context outside the timed region: the separate sync (mean, broadcast and
@@ -210,7 +211,8 @@ def main():
         out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w),
                            "kernel": f"k_local_step<{step_block}>",
-                           "lds_reserved_per_block": step_lds, "bytes_per_launch": step_bytes,
+                           "lds_reserved_per_block": step_lds, "row_stride": row_stride,
+                           "bytes_per_launch": step_bytes,
                            "avg_launch_ms": step_ms, "timed_launches": tm.step_launches,
                            "timed_every": args.timing_every}
         if tm.fused_launches > 0:

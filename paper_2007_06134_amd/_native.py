@@ -45,6 +45,7 @@ class adpsgd_buffers(C.Structure):
     _fields_ = [
         ("x", C.c_void_p), ("m", C.c_void_p), ("h", C.c_void_p), ("xstar", C.c_void_p),
         ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t), ("stream", C.c_void_p),
+        ("row_stride", C.c_int64),
     ]
 
 

@@ -134,7 +134,8 @@ __device__ __forceinline__ double grad_norm2(const StepParams &a, f4 mean, f4 h,
 // over the 8 XCDs): h and x* of the chunk come from HBM once and from that
 // XCD's L2 for the other K-1 workers.  The best BS depends on the shape and
 // the machine (64, 128 and 256 each win somewhere); the runtime times them.
-template <int BS, bool VEC, bool NT>
+// TAIL: P is not a multiple of 4, so the last group of every row is partial.
+template <int BS, bool VEC, bool NT, bool TAIL>
 __global__ void __launch_bounds__(BS) k_local_step(StepParams a) {
     const int64_t b = a.block0 + blockIdx.x;
     const int64_t s = b >> 3;                        // position within the XCD
@@ -143,17 +144,18 @@ __global__ void __launch_bounds__(BS) k_local_step(StepParams a) {
     const int64_t g = chunk * BS + threadIdx.x;
     if (g >= a.n_groups) return;
     const int64_t e0 = 4 * g;
-    float *xr = a.x + (int64_t)k * a.P + e0;
-    float *mr = a.m + (int64_t)k * a.P + e0;
-    if constexpr (VEC) {
+    float *xr = a.x + (int64_t)k * a.ld + e0;
+    float *mr = a.m + (int64_t)k * a.ld + e0;
+    if (VEC && (!TAIL || e0 + 4 <= a.P)) {
         f4 x = ld4<NT>(xr), m = ld4<NT>(mr);
         const f4 h = ld4<false>(a.h + e0), xs = ld4<false>(a.xs + e0);
         sgd_update(a, x, m, h, xs, step_noise(a, g, k));
         st4<NT>(xr, x);
         st4<NT>(mr, m);
     } else {
-        // P not a multiple of 4: rows are not 16-byte aligned; scalar accesses,
-        // masked to [0, P) in the ragged last group
+        // the ragged last group of a row, or rows that are not 16-byte aligned
+        // (a row stride that is not a multiple of 4): scalar accesses, masked
+        // to [0, P)
         f4 x = ld4_masked(xr, e0, 0, a.P), m = ld4_masked(mr, e0, 0, a.P);
         const f4 h = ld4_masked(a.h + e0, e0, 0, a.P), xs = ld4_masked(a.xs + e0, e0, 0, a.P);
         sgd_update(a, x, m, h, xs, step_noise(a, g, k));
@@ -249,10 +251,10 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         f4 m[R];
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-            float *xrow = a.x + (int64_t)(R * w + r) * a.P + e0;
+            float *xrow = a.x + (int64_t)(R * w + r) * a.ld + e0;
             xr[r] = full ? ld4<NT>(xrow) : ld4_masked(xrow, e0, lo, hi);
             if (STEP || AVGM) {
-                float *mrow = a.m + (int64_t)(R * w + r) * a.P + e0;
+                float *mrow = a.m + (int64_t)(R * w + r) * a.ld + e0;
                 m[r] = full ? ld4<NT>(mrow) : ld4_masked(mrow, e0, lo, hi);
             }
         }
@@ -266,11 +268,11 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
                 const int k = R * w + r;
                 sgd_update(a, xr[r], m[r], h, xs, step_noise(a, g, k));
                 if (!avg_m) {
-                    float *mrow = a.m + (int64_t)k * a.P + e0;
+                    float *mrow = a.m + (int64_t)k * a.ld + e0;
                     if (full) st4<NT>(mrow, m[r]); else st4_masked(mrow, m[r], e0, lo, hi);
                 }
                 if (!bcast) {     // no sync: the replicas keep their new values
-                    float *xrow = a.x + (int64_t)k * a.P + e0;
+                    float *xrow = a.x + (int64_t)k * a.ld + e0;
                     if (full) st4<NT>(xrow, xr[r]); else st4_masked(xrow, xr[r], e0, lo, hi);
                 }
             }
@@ -293,7 +295,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             if (!full) d2 = mask4(d2, e0, lo, hi);
             acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
             if (bcast) {
-                float *xrow = a.x + (int64_t)(R * w + r) * a.P + e0;
+                float *xrow = a.x + (int64_t)(R * w + r) * a.ld + e0;
                 if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
             }
         }
@@ -301,7 +303,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             const f4 mmean = tree_sum_lds<W>(mpart, lane, 0) / splat((float)KT);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
-                float *mrow = a.m + (int64_t)(R * w + r) * a.P + e0;
+                float *mrow = a.m + (int64_t)(R * w + r) * a.ld + e0;
                 if (full) st4<NT>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
             }
         }
@@ -344,8 +346,8 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
         }
         f4 s = splat(0.0f), sm = splat(0.0f);
         for (int k = 0; k < a.K; ++k) {
-            float *xrow = a.x + (int64_t)k * a.P + e0;
-            float *mrow = a.m + (int64_t)k * a.P + e0;
+            float *xrow = a.x + (int64_t)k * a.ld + e0;
+            float *mrow = a.m + (int64_t)k * a.ld + e0;
             f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
             f4 m = splat(0.0f);
             if (STEP || AVGM) m = full ? ld4<false>(mrow) : ld4_masked(mrow, e0, lo, hi);
@@ -361,7 +363,7 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
             const f4 mean = s / splat((float)a.K);
             const f4 mmean = sm / splat((float)a.K);
             for (int k = 0; k < a.K; ++k) {
-                float *xrow = a.x + (int64_t)k * a.P + e0;
+                float *xrow = a.x + (int64_t)k * a.ld + e0;
                 const f4 x = full ? ld4<false>(xrow) : ld4_masked(xrow, e0, lo, hi);
                 // squared deviations in fp32 per element, each row's sum in fp64
                 const f4 dk = mean - x;
@@ -370,7 +372,7 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
                 acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
                 if (bcast) { if (full) st4<false>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi); }
                 if (avg_m) {
-                    float *mrow = a.m + (int64_t)k * a.P + e0;
+                    float *mrow = a.m + (int64_t)k * a.ld + e0;
                     if (full) st4<false>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
                 }
             }
@@ -559,6 +561,18 @@ __global__ void __launch_bounds__(kBlock) k_init_problem(float *h, float *xs, in
     st4_masked(xs + e0, xv, e0, 0, P);
 }
 
+// Thread = one float4 group of one row: j = k * groups_per_row + g.
+template <bool VEC>
+__global__ void __launch_bounds__(kBlock) k_zero_rows(float *a, int64_t ld, int64_t P, int64_t groups_per_row,
+                                                      int64_t j0, int64_t n) {
+    const int64_t j = j0 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (j >= n) return;
+    const int64_t k = j / groups_per_row, e0 = 4 * (j - k * groups_per_row);
+    float *row = a + k * ld + e0;
+    if (VEC && e0 + 4 <= P) st4<false>(row, splat(0.0f));
+    else st4_masked(row, splat(0.0f), e0, 0, P);
+}
+
 __global__ void __launch_bounds__(kBlock) k_philox_dump(RoundKeys rk, uint32_t c1, uint32_t c2, uint32_t c3,
                                                         int64_t g0, int64_t n, uint32_t *out) {
     const int64_t j = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -693,9 +707,12 @@ hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, int lds, hipStr
     return in_pieces(local_step_blocks(p.n_groups, p.K, BS), BS, [&](int64_t b0, unsigned nb) {
         StepParams q = p;
         q.block0 = b0;
-        if (vec && nt) k_local_step<BS, true, true><<<dim3(nb), dim3(BS), lds, st>>>(q);
-        else if (vec) k_local_step<BS, true, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
-        else k_local_step<BS, false, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        const bool tail = (p.P & 3) != 0;
+        if (vec && nt && tail) k_local_step<BS, true, true, true><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else if (vec && nt) k_local_step<BS, true, true, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else if (vec && tail) k_local_step<BS, true, false, true><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else if (vec) k_local_step<BS, true, false, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
+        else k_local_step<BS, false, false, false><<<dim3(nb), dim3(BS), lds, st>>>(q);
     });
 }
 
@@ -757,6 +774,15 @@ hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, do
     const RoundKeys rk = round_keys(seed);
     return groups_in_pieces((P + 3) / 4, [&](int64_t g0, int64_t, unsigned nb) {
         k_init_problem<<<dim3(nb), dim3(kBlock), 0, st>>>(h, xs, P, rk, (float)llo, (float)(lhi - llo), g0);
+    });
+}
+
+hipError_t launch_zero_rows(float *a, int64_t ld, int64_t P, int32_t K, bool vec, hipStream_t st) {
+    if (P <= 0 || K <= 0) return hipSuccess;
+    const int64_t gpr = (P + 3) / 4, n = gpr * K;
+    return groups_in_pieces(n, [&](int64_t j0, int64_t, unsigned nb) {
+        if (vec) k_zero_rows<true><<<dim3(nb), dim3(kBlock), 0, st>>>(a, ld, P, gpr, j0, n);
+        else k_zero_rows<false><<<dim3(nb), dim3(kBlock), 0, st>>>(a, ld, P, gpr, j0, n);
     });
 }
 

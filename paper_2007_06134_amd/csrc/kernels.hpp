@@ -45,6 +45,7 @@ struct StepParams {
     float *m;
     const float *h;
     const float *xs;
+    int64_t ld;        // row stride of x and m in elements (>= P)
     int64_t P;
     int64_t n_groups;  // ceil(P / 4)
     int32_t K;
@@ -83,7 +84,7 @@ constexpr int kMaxStepLds = 64 * 1024;
 // held to 20 per CU (8 KB each).
 constexpr StepShape kStepShapes[] = {{64, 0}, {64, 8192}, {128, 0}, {256, 0}};
 int64_t local_step_blocks(int64_t n_groups, int32_t K, int block);
-// vec: rows are 16-byte aligned (P % 4 == 0) so full groups use dwordx4;
+// vec: rows are 16-byte aligned (row stride % 4 == 0) so full groups use dwordx4;
 // block: one of kStepBlocks, lds in [0, kMaxStepLds] (hipErrorInvalidValue otherwise).
 hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, int block, int lds, hipStream_t st);
 // What a sync-tile kernel does:
@@ -146,6 +147,9 @@ struct ReduceParams {
 // Segmented fixed-order sums of the tile partials (chunks, then tensors, then
 // over tensors) and, with a schedule, Algorithm 2's lines 13-19 on the result.
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st);
+// Zero elements [0, P) of each of the K rows of a (rows ld apart); vec: ld is
+// a multiple of 4 and a 16-byte aligned, so whole groups take one store.
+hipError_t launch_zero_rows(float *a, int64_t ld, int64_t P, int32_t K, bool vec, hipStream_t st);
 hipError_t launch_init_problem(float *h, float *xs, int64_t P, uint64_t seed, double h_lo,
                                double h_hi, hipStream_t st);
 hipError_t launch_philox_dump(uint64_t seed, uint32_t c1, uint32_t c2, uint32_t c3, int64_t g0,

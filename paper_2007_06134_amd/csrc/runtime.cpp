@@ -164,6 +164,7 @@ using namespace adpsgd;
 struct adpsgd_ctx {
     int32_t K = 0;
     int64_t P = 0;
+    int64_t ld = 0;                 // row stride of x and m (elements)
     int32_t T = 0;
     std::vector<int64_t> offsets;
     std::vector<Tile> tiles;
@@ -189,7 +190,7 @@ struct adpsgd_ctx {
     size_t slot_bytes = 0;
     hipEvent_t ring_ev[kRing] = {};
     adpsgd_state st{};
-    bool vec = true;                // P % 4 == 0: dwordx4 rows
+    bool vec = true;                // row stride % 4 == 0: rows 16-byte aligned, dwordx4 groups
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
     StepShape step_shape{256, 0};   // launch shape of the plain local step in use
@@ -303,6 +304,7 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
     p.m = c->buf.m;
     p.h = c->buf.h;
     p.xs = c->buf.xstar;
+    p.ld = c->ld;
     p.P = c->P;
     p.n_groups = (c->P + 3) / 4;
     p.K = c->K;
@@ -423,6 +425,14 @@ struct Range {
     Range &operator=(const Range &) = delete;
 };
 
+// Zero the K rows of x and m (P elements each, row_stride apart; the padding
+// between rows is the caller's and is left alone), with a fill kernel.
+hipError_t zero_rows(const adpsgd_ctx *c) {
+    hipError_t e = launch_zero_rows(c->buf.x, c->ld, c->P, c->K, c->vec, c->stream);
+    if (e == hipSuccess) e = launch_zero_rows(c->buf.m, c->ld, c->P, c->K, c->vec, c->stream);
+    return e;
+}
+
 // Time the local step in every launch shape on the context's own buffers (the
 // launches step x and m, which the caller zeroes afterwards): one warm-up
 // launch each, then five interleaved rounds; the fastest minimum wins.
@@ -519,6 +529,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be non-NULL");
     if (!aligned(buf->x, 16) || !aligned(buf->m, 16) || !aligned(buf->h, 16) || !aligned(buf->xstar, 16))
         return fail(ADPSGD_EINVAL, "x, m, h and xstar must be 16-byte aligned");
+    if (buf->row_stride < 0 || (buf->row_stride > 0 && buf->row_stride < P))
+        return fail(ADPSGD_EINVAL, "row_stride must be 0 or >= P");
     const Plan plan = count_plan(T, offsets);
     // tile indices are 32-bit in the chunk table (P / 4 < 2^32 keeps them far below)
     if (plan.n_tiles >= (int64_t(1) << 31)) return fail(ADPSGD_EINVAL, "too many sync tiles");
@@ -538,7 +550,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->hp = *hp;
     c->buf = *buf;
     c->stream = (hipStream_t)buf->stream;
-    c->vec = (P % 4) == 0;
+    c->ld = buf->row_stride > 0 ? buf->row_stride : P;
+    c->vec = (c->ld % 4) == 0;
     // x and m beyond the 256 MB last-level cache: stream them past the caches
     c->nontemporal = (double)K * (double)P * 8.0 > 256.0 * 1024 * 1024;
     c->rk = round_keys(hp->seed);
@@ -592,14 +605,11 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if (P > 0) {
         if ((e = launch_init_problem(buf->h, buf->xstar, P, hp->seed, hp->h_lo, hp->h_hi, c->stream)) != hipSuccess)
             return bail(e, "init_problem launch");
-        const size_t bytes = sizeof(float) * (size_t)K * (size_t)P;
-        if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
-        if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
+        if ((e = zero_rows(c)) != hipSuccess) return bail(e, "zero x and m");
         if ((double)K * (double)P >= kTuneMinElems) {
             if ((e = tune_step_shape(c)) != hipSuccess) return bail(e, "time the local step");
             if ((e = tune_average_cap(c)) != hipSuccess) return bail(e, "time the separate sync");
-            if ((e = hipMemsetAsync(buf->x, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero x");
-            if ((e = hipMemsetAsync(buf->m, 0, bytes, c->stream)) != hipSuccess) return bail(e, "zero m");
+            if ((e = zero_rows(c)) != hipSuccess) return bail(e, "zero x and m");
         }
     }
     if ((e = hipStreamSynchronize(c->stream)) != hipSuccess) return bail(e, "hipStreamSynchronize");
@@ -616,11 +626,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
 extern "C" int adpsgd_reset(adpsgd_ctx *c) {
     if (int rc = check_ctx(c)) return rc;
     DeviceScope dev_(c);
-    if (c->P > 0) {
-        const size_t bytes = sizeof(float) * (size_t)c->K * (size_t)c->P;
-        HIP_TRY(hipMemsetAsync(c->buf.x, 0, bytes, c->stream));
-        HIP_TRY(hipMemsetAsync(c->buf.m, 0, bytes, c->stream));
-    }
+    HIP_TRY(zero_rows(c));
     c->st = adpsgd_state{};
     c->st.p = c->hp.p_init;
     return ok();

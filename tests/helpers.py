@@ -34,11 +34,11 @@ def rel_err(a, b, floor: float = 1e-300) -> float:
     return float(np.max(np.abs(a - b) / np.maximum(np.abs(b), floor)))
 
 
-def gpu_run(w, n_steps=None, fetch=True, policy=None):
+def gpu_run(w, n_steps=None, fetch=True, policy=None, pad_rows=True):
     """Run workload w on cuda:0 through the C ABI; returns a dict of host results."""
     import paper_2007_06134_amd as A
     n = w.total_steps if n_steps is None else n_steps
-    with A.Adpsgd.from_workload(w) as eng:
+    with A.Adpsgd.from_workload(w, pad_rows=pad_rows) as eng:
         if policy is not None:
             eng.set_launch_policy(policy)
         recs, var, n_syncs = eng.run(n)

@@ -230,6 +230,29 @@ def test_reduction_paths_match_oracle(A, n_tiles, max_size):
     assert max_rel_err(g["m"], r.v, off, floor=MOM_FLOOR) < MOM_TOL
 
 
+@pytest.mark.parametrize("extra", [1, 2, 3])
+@pytest.mark.parametrize("key", ["resnet18_like", "many_small"])
+def test_padded_and_packed_rows_match_oracle(A, key, extra):
+    """P not a multiple of 4: rows padded to a multiple of 4 elements (whole
+    float4 groups move with vector accesses, the last group of each row
+    masked) and rows packed back to back (scalar accesses) give the same bits
+    and match the oracle."""
+    w0 = W.parity_workloads()[key]
+    sizes = list(w0.sizes)
+    sizes[-1] += extra
+    w = w0.replace(sizes=tuple(sizes), total_steps=60, k_s=15)
+    assert w.P % 4 == extra
+    _say(f"rows {key}: K={w.K} P={w.P}")
+    gp, gk = gpu_run(w, pad_rows=True), gpu_run(w, pad_rows=False)
+    assert gp["recs"].tobytes() == gk["recs"].tobytes() and gp["var"].tobytes() == gk["var"].tobytes()
+    assert np.array_equal(gp["x"], gk["x"]) and np.array_equal(gp["m"], gk["m"])
+    r = oracle.Oracle(w).run()
+    assert np.array_equal(gp["recs"]["t"], r.sync_t) and np.array_equal(gp["recs"]["p"], r.sync_p)
+    assert rel_err(gp["var"], r.var, floor=1e-300) < VAR_TOL
+    assert max_rel_err(gp["x"], r.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(gp["m"], r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
+
+
 def test_period_one_replicas_stay_identical(A):
     w = _tiny(K=8, sizes=(6000, 2001), p_init=1, total_steps=12)
     with A.Adpsgd.from_workload(w) as eng:
