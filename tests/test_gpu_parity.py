@@ -472,6 +472,34 @@ def test_side_streams_and_concurrent_contexts_agree_bitwise(A):
         assert [out.get(j) for j in range(len(ws))] == base
 
 
+@pytest.mark.parametrize("mode", [W.PERIOD_CONST, W.PERIOD_ADAPTIVE])
+def test_last_steps_before_the_counter_limit(A, mode):
+    """Steps up to t = 2^32 - 1 (the last value of the Philox counter word that
+    holds the step) match the oracle from a restored state; one step more is
+    refused and leaves the context unchanged."""
+    import oracle.oracle as OO
+    w = _tiny(K=4, sizes=(3001, 17), period_mode=mode, p_init=3, k_s=0, total_steps=1000)
+    t0 = 2**32 - 20
+    with A.Adpsgd.from_workload(w) as eng:
+        st = eng.get_state()
+        st.t, st.cnt, st.p, st.C2, st.nC2 = t0, 1, 3, 2e-4, 5
+        eng.set_state(st)
+        recs, var, n = eng.run(20)
+        assert eng.get_state().t == 2**32
+        with pytest.raises(A.AdpsgdError) as e:
+            eng.local_steps(1)
+        assert e.value.code == A.EINVAL and eng.get_state().t == 2**32
+        x = eng.x.double().cpu().numpy()
+        m = eng.m.double().cpu().numpy()
+    o = oracle.Oracle(w)
+    ost = OO._State(t=t0, cnt=1, nC2=5, C2=2e-4, p=3)
+    r = o.run(n_steps=20, state=ost)
+    assert n == r.n_syncs and np.array_equal(recs["t"], r.sync_t) and np.array_equal(recs["p"], r.sync_p)
+    assert rel_err(var, r.var, floor=1e-300) < VAR_TOL
+    assert max_rel_err(x, r.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(m, r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
+
+
 def test_checkpoint_resume_is_bit_exact(A):
     import torch
     w = W.parity_workloads()["resnet18_like"].replace(total_steps=700, k_s=150)
