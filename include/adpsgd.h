@@ -241,7 +241,8 @@ ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
  * records) and var_log (host, [log_cap][T], may be NULL) receive the first
  * log_cap syncs; *n_syncs (may be NULL) the count of all syncs.  No sync is
  * forced at the end.  Returns when all enqueued work has finished.  On
- * ENONFINITE the run stops at that sync; steps already enqueued after it
+ * ENONFINITE the run stops at that sync, whose update of p and C2 is withheld
+ * (its counter restarts, as at every sync); steps already enqueued after it
  * complete (with their syncs, logged) and are counted in the state. */
 ADPSGD_API int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
                double *var_log, int64_t *n_syncs);

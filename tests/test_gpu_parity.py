@@ -627,6 +627,31 @@ def test_divergence_reports_non_finite_variance(A):
         assert st.p == 40 and st.t >= 40
 
 
+@pytest.mark.parametrize("traced", [False, True])
+@pytest.mark.parametrize("policy", ["hybrid", "device", "host"])
+@pytest.mark.parametrize("mode", [W.PERIOD_CONST, W.PERIOD_ADAPTIVE, W.PERIOD_ALG1])
+def test_divergence_under_every_policy(A, mode, policy, traced):
+    """A diverging run (non-finite S) returns ENONFINITE, as the oracle does,
+    under every launch policy, period mode and with tracing: the failing
+    sync's update of p and C2 is withheld but its counter restarts, so the
+    state stays consistent (cnt <= p), and the context stays usable."""
+    pol = {"hybrid": A.LAUNCH_HYBRID, "device": A.LAUNCH_DEVICE, "host": A.LAUNCH_HOST}[policy]
+    for K, p_init in ((3, 1), (8, 5)):
+        w = _tiny(K=K, sizes=(3000, 5), lr0=50.0, p_init=p_init, total_steps=300, period_mode=mode, k_s=0)
+        with pytest.raises(RuntimeError, match="-4"):
+            oracle.Oracle(w).run()
+        with A.Adpsgd.from_workload(w) as eng:
+            eng.set_launch_policy(pol)
+            with pytest.raises(A.AdpsgdError) as e:
+                eng.run_traced(300) if traced else eng.run(300)
+            assert e.value.code == A.ENONFINITE
+            st = eng.get_state()
+            assert 0 < st.t <= 300 and st.cnt <= st.p
+            eng.reset()
+            recs, _, n = eng.run(5)
+            assert eng.get_state().t == 5
+
+
 def test_invalid_calls_leave_context_unchanged(A):
     import torch
     w = _tiny(K=2, sizes=(1024,))
