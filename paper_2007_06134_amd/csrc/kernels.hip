@@ -436,20 +436,86 @@ __global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
     }
 }
 
-// Level 2 and the decision, one block.  Per-tensor sums of the chunk
-// partials, in a fixed order chosen by the tensor's chunk count: a tensor of
-// at most kSmallTensorChunks chunks is owned by one thread, which adds its
-// chunks from LDS (the partials pass through LDS in windows of kFinishWindow;
-// four interleaved partial sums, carried across windows in the device scratch
-// acc); a larger tensor is owned by one wave, whose lanes add strided chunks
-// (from LDS when all of them fit in one window, else from memory) before a
-// butterfly.  Then out[tau] = variance (deviation sum /
-// K), out[T + tau] = gradient norm^2; S and the norm total are block sums;
-// with a schedule, thread 0 applies Algorithm 2's lines 13-19 (the same
-// apply_sync as the host controller) and writes the new state.  out and the
-// record header are the host's pinned record slot, written directly; the
-// header is written in every case.
 constexpr int kFinishThreads = 256;
+
+// Level 2 for problems with more chunk partials than one LDS window: one block
+// per window of tensors.  A window of small tensors loads its chunk partials
+// (at most kFinishWindow) into LDS and gives each tensor to a thread, which
+// adds its chunks in a fixed order (four interleaved partial sums); a window
+// holding one large tensor adds its chunks strided over the block.  Writes
+// out[tau] = variance (deviation sum / K) and out[T + tau] = gradient norm^2
+// for its tensors, and the window's sums in a fixed order to win_partials.
+__global__ void __launch_bounds__(kFinishThreads) k_reduce_windows(ReduceParams r) {
+    __shared__ double la[kFinishWindow], lb[kFinishWindow];
+    int32_t p_t;
+    SchedState st;
+    if (!reduce_due(r, &p_t, &st) && !r.traced) return;
+    const int32_t w = blockIdx.x;
+    const int32_t t0 = r.win_begin[w], t1 = r.win_begin[w + 1];
+    const int32_t c0 = r.chunk_begin[t0], c1 = r.chunk_begin[t1];
+    if (t1 == t0 + 1 && c1 - c0 > kSmallTensorChunks) {  // one large tensor
+        double a = 0.0, g = 0.0;
+        for (int32_t i = c0 + (int32_t)threadIdx.x; i < c1; i += kFinishThreads) {
+            a += r.chunk_partials[2 * (int64_t)i];
+            g += r.chunk_partials[2 * (int64_t)i + 1];
+        }
+        const Pair tot = block_sum2<kFinishThreads / 64>(a, g);
+        if (threadIdx.x == 0) {
+            const double v = tot.a / (double)r.K;
+            r.out[t0] = v;
+            r.out[r.T + t0] = tot.b;
+            r.win_partials[2 * w] = v;
+            r.win_partials[2 * w + 1] = tot.b;
+        }
+        return;
+    }
+    const int32_t n = c1 - c0;  // <= kFinishWindow (the host cut the window so)
+    for (int32_t i = (int32_t)threadIdx.x; i < n; i += kFinishThreads) {
+        la[i] = r.chunk_partials[2 * (int64_t)(c0 + i)];
+        lb[i] = r.chunk_partials[2 * (int64_t)(c0 + i) + 1];
+    }
+    __syncthreads();
+    double sa = 0.0, sb = 0.0;
+    for (int32_t tau = t0 + (int32_t)threadIdx.x; tau < t1; tau += kFinishThreads) {
+        const int32_t b = r.chunk_begin[tau] - c0, e = r.chunk_begin[tau + 1] - c0;
+        double a[4] = {0.0, 0.0, 0.0, 0.0}, g[4] = {0.0, 0.0, 0.0, 0.0};
+        int32_t i = b;
+        for (; i + 4 <= e; i += 4) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                a[j] += la[i + j];
+                g[j] += lb[i + j];
+            }
+        }
+        if (i < e) { a[0] += la[i]; g[0] += lb[i]; }
+        if (i + 1 < e) { a[1] += la[i + 1]; g[1] += lb[i + 1]; }
+        if (i + 2 < e) { a[2] += la[i + 2]; g[2] += lb[i + 2]; }
+        const double v = e > b ? ((a[0] + a[1]) + (a[2] + a[3])) / (double)r.K : 0.0;
+        const double gn = e > b ? (g[0] + g[1]) + (g[2] + g[3]) : 0.0;
+        r.out[tau] = v;
+        r.out[r.T + tau] = gn;
+        sa += v;
+        sb += gn;
+    }
+    const Pair tot = block_sum2<kFinishThreads / 64>(sa, sb);
+    if (threadIdx.x == 0) {
+        r.win_partials[2 * w] = tot.a;
+        r.win_partials[2 * w + 1] = tot.b;
+    }
+}
+
+// Level 2 and the decision, one block.  With at most kFinishWindow chunk
+// partials (n_windows = 0) it sums the tensors itself, in a fixed order chosen
+// by the tensor's chunk count: a tensor of at most kSmallTensorChunks chunks is
+// owned by one thread, which adds its chunks from LDS (four interleaved partial
+// sums); a larger tensor is owned by one wave, whose lanes add strided chunks
+// from LDS before a butterfly; then out[tau] = variance (deviation sum / K),
+// out[T + tau] = gradient norm^2, and S and the norm total are block sums.
+// Otherwise k_reduce_windows has written out, and S and the norm total are
+// block sums of its window partials.  With a schedule, thread 0 then applies
+// Algorithm 2's lines 13-19 (the same apply_sync as the host controller) and
+// writes the new state.  out and the record header are the host's pinned
+// record slot, written directly; the header is written in every case.
 __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r) {
     __shared__ double la[kFinishWindow], lb[kFinishWindow];
     int32_t p_t;
@@ -459,20 +525,26 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r
         if (threadIdx.x == 0) write_hdr(r, 0, p_t, p_t, ADPSGD_OK, 0.0, 0.0, st);
         return;
     }
-    // small tensors: a thread each, from LDS
-    for (int32_t w0 = 0; w0 < r.n_chunks; w0 += kFinishWindow) {
-        const int32_t n = min(kFinishWindow, r.n_chunks - w0);
-        __syncthreads();  // the previous window has been consumed
+    double sa = 0.0, sb = 0.0;
+    if (r.n_windows > 0) {
+        // the tensors were reduced by k_reduce_windows: add the window sums
+        for (int32_t w = (int32_t)threadIdx.x; w < r.n_windows; w += kFinishThreads) {
+            sa += r.win_partials[2 * w];
+            sb += r.win_partials[2 * w + 1];
+        }
+    } else {
+        // every chunk partial fits one LDS window (the host cuts the tensors
+        // into windows for k_reduce_windows otherwise)
+        const int32_t n = r.n_chunks;
         for (int32_t i = (int32_t)threadIdx.x; i < n; i += kFinishThreads) {
-            la[i] = r.chunk_partials[2 * (int64_t)(w0 + i)];
-            lb[i] = r.chunk_partials[2 * (int64_t)(w0 + i) + 1];
+            la[i] = r.chunk_partials[2 * (int64_t)i];
+            lb[i] = r.chunk_partials[2 * (int64_t)i + 1];
         }
         __syncthreads();
+        // small tensors: a thread each
         for (int32_t tau = (int32_t)threadIdx.x; tau < r.T; tau += kFinishThreads) {
-            const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
-            if (ce - cb > kSmallTensorChunks) continue;
-            const int32_t b = max(cb, w0) - w0, e = min(ce, w0 + n) - w0;
-            if (b >= e) continue;
+            const int32_t b = r.chunk_begin[tau], e = r.chunk_begin[tau + 1];
+            if (e - b > kSmallTensorChunks || b >= e) continue;
             double a[4] = {0.0, 0.0, 0.0, 0.0}, g[4] = {0.0, 0.0, 0.0, 0.0};
             int32_t i = b;
             for (; i + 4 <= e; i += 4) {
@@ -485,49 +557,42 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r
             if (i < e) { a[0] += la[i]; g[0] += lb[i]; }
             if (i + 1 < e) { a[1] += la[i + 1]; g[1] += lb[i + 1]; }
             if (i + 2 < e) { a[2] += la[i + 2]; g[2] += lb[i + 2]; }
-            double sa = (a[0] + a[1]) + (a[2] + a[3]), sg = (g[0] + g[1]) + (g[2] + g[3]);
-            if (w0 > cb) {  // continued from an earlier window
-                sa += r.acc[tau];
-                sg += r.acc[r.T + tau];
+            r.acc[tau] = (a[0] + a[1]) + (a[2] + a[3]);
+            r.acc[r.T + tau] = (g[0] + g[1]) + (g[2] + g[3]);
+        }
+        // large tensors (listed by the host): a wave each, strided lanes, then
+        // a butterfly
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        for (int32_t j = wave; j < r.n_large; j += kFinishThreads / 64) {
+            const int32_t tau = r.large[j];
+            const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
+            double a = 0.0, g = 0.0;
+            for (int32_t i = cb + lane; i < ce; i += 64) {
+                a += la[i];
+                g += lb[i];
             }
-            r.acc[tau] = sa;
-            r.acc[r.T + tau] = sg;
-        }
-    }
-    // large tensors (listed by the host): a wave each, from LDS when every
-    // chunk partial fits in the one window, else from memory
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const bool in_lds = r.n_chunks <= kFinishWindow;
-    for (int32_t j = wave; j < r.n_large; j += kFinishThreads / 64) {
-        const int32_t tau = r.large[j];
-        const int32_t cb = r.chunk_begin[tau], ce = r.chunk_begin[tau + 1];
-        double a = 0.0, g = 0.0;
-        for (int32_t i = cb + lane; i < ce; i += 64) {
-            a += in_lds ? la[i] : r.chunk_partials[2 * (int64_t)i];
-            g += in_lds ? lb[i] : r.chunk_partials[2 * (int64_t)i + 1];
-        }
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            a += __shfl_xor(a, off, 64);
-            g += __shfl_xor(g, off, 64);
+            for (int off = 32; off >= 1; off >>= 1) {
+                a += __shfl_xor(a, off, 64);
+                g += __shfl_xor(g, off, 64);
+            }
+            if (lane == 0) {
+                r.acc[tau] = a;
+                r.acc[r.T + tau] = g;
+            }
         }
-        if (lane == 0) {
-            r.acc[tau] = a;
-            r.acc[r.T + tau] = g;
+        __syncthreads();  // acc of the large tensors, for their owner threads below
+        for (int32_t tau = (int32_t)threadIdx.x; tau < r.T; tau += kFinishThreads) {
+            double v = 0.0, g = 0.0;
+            if (r.chunk_begin[tau + 1] > r.chunk_begin[tau]) {
+                v = r.acc[tau] / (double)r.K;
+                g = r.acc[r.T + tau];
+            }
+            r.out[tau] = v;
+            r.out[r.T + tau] = g;
+            sa += v;
+            sb += g;
         }
-    }
-    __syncthreads();  // acc of the large tensors, for their owner threads below
-    double sa = 0.0, sb = 0.0;
-    for (int32_t tau = (int32_t)threadIdx.x; tau < r.T; tau += kFinishThreads) {
-        double v = 0.0, g = 0.0;
-        if (r.chunk_begin[tau + 1] > r.chunk_begin[tau]) {
-            v = r.acc[tau] / (double)r.K;
-            g = r.acc[r.T + tau];
-        }
-        r.out[tau] = v;
-        r.out[r.T + tau] = g;
-        sa += v;
-        sb += g;
     }
     const Pair tot = block_sum2<kFinishThreads / 64>(sa, sb);
     if (threadIdx.x == 0) {
@@ -763,6 +828,11 @@ hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {
             q.block0 = (int32_t)b0;
             k_reduce_chunks<<<dim3(nb), dim3(kBlock), 0, st>>>(q);
         });
+        if (e != hipSuccess) return e;
+    }
+    if (r.n_windows > 0) {
+        k_reduce_windows<<<dim3((unsigned)r.n_windows), dim3(kFinishThreads), 0, st>>>(r);
+        const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     k_reduce_finish<<<dim3(1), dim3(kFinishThreads), 0, st>>>(r);

@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "rng.hpp"
 #include "schedule.hpp"
 
@@ -135,6 +137,14 @@ struct ReduceParams {
     int32_t n_chunks, T, K, n_large;
     int32_t chunks_are_tiles;     // 1: chunk_partials is tile_partials (one tile per chunk)
     int32_t block0;               // first chunk of this launch of the chunk sums (set by launch_reduce)
+    // More chunk partials than one LDS window: the tensors are cut into
+    // windows (a run of whole small tensors whose chunks fit one window, or one
+    // large tensor), reduced by one block each; the finishing block then sums
+    // the window partials.  n_windows = 0: one block does everything.
+    const int32_t *win_begin;     // [n_windows + 1]: first tensor of each window
+    double *win_partials;         // [2 n_windows]: per window, sum of variances, of gradient norms^2
+    int32_t n_windows;
+    int32_t pad2_;
     double *out;                  // [2T]: variance per tensor, then gradient norm^2 (may be mapped host memory)
     SlotHdr *hdr;                 // (may be mapped host memory)
     SchedState *sched;            // non-null: the step's sync is decided and controlled here
@@ -146,6 +156,8 @@ struct ReduceParams {
 
 // Segmented fixed-order sums of the tile partials (chunks, then tensors, then
 // over tensors) and, with a schedule, Algorithm 2's lines 13-19 on the result.
+// Windows of tensors (ReduceParams::win_begin) are cut by the host:
+int32_t reduce_windows(int32_t T, const int32_t *chunk_begin, std::vector<int32_t> *win_begin);
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st);
 // Zero elements [0, P) of each of the K rows of a (rows ld apart); vec: ld is
 // a multiple of 4 and a 16-byte aligned, so whole groups take one store.

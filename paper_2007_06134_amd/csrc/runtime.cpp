@@ -35,6 +35,34 @@ int ok() {
     return ADPSGD_OK;
 }
 
+// Windows of tensors for the second level of the variance sum when there are
+// more chunk partials than one LDS window holds: runs of whole small tensors
+// (at most kSmallTensorChunks chunks each) whose chunks fit kFinishWindow, and
+// every larger tensor alone.  win_begin receives the first tensor of each
+// window and T; returns the window count (0, with win_begin empty, when one
+// window holds every chunk partial).
+int32_t reduce_windows(int32_t T, const int32_t *chunk_begin, std::vector<int32_t> *win_begin) {
+    win_begin->clear();
+    if (chunk_begin[T] <= kFinishWindow) return 0;
+    win_begin->push_back(0);
+    int32_t cur = 0;  // chunks in the current run of small tensors
+    for (int32_t tau = 0; tau < T; ++tau) {
+        const int32_t c = chunk_begin[tau + 1] - chunk_begin[tau];
+        if (c > kSmallTensorChunks) {
+            if (tau > win_begin->back()) win_begin->push_back(tau);
+            win_begin->push_back(tau + 1);
+            cur = 0;
+        } else if (cur + c > kFinishWindow) {
+            win_begin->push_back(tau);
+            cur = c;
+        } else {
+            cur += c;
+        }
+    }
+    if (win_begin->back() < T) win_begin->push_back(T);
+    return (int32_t)win_begin->size() - 1;
+}
+
 namespace {
 
 constexpr int kRing = 32;          // record slots: launches with a reduction in flight at once
@@ -85,14 +113,21 @@ int64_t tiles_of(int64_t a, int64_t b) { return b > a ? (b + kTileElems - 1) / k
 struct Plan {
     int64_t n_tiles = 0, n_chunks = 0;
     int32_t chunk_tiles = kChunkTiles;
+    int32_t n_windows = 0;  // windows of tensors for k_reduce_windows (0: none)
 };
 
 Plan count_plan(int32_t T, const int64_t *off) {
     Plan pl;
     for (int32_t tau = 0; tau < T; ++tau) pl.n_tiles += tiles_of(off[tau], off[tau + 1]);
     pl.chunk_tiles = pl.n_tiles <= kDirectMaxTiles ? 1 : kChunkTiles;
-    for (int32_t tau = 0; tau < T; ++tau)
-        pl.n_chunks += (tiles_of(off[tau], off[tau + 1]) + pl.chunk_tiles - 1) / pl.chunk_tiles;
+    std::vector<int32_t> chunk_begin(T + 1, 0);
+    for (int32_t tau = 0; tau < T; ++tau) {
+        const int64_t n = (tiles_of(off[tau], off[tau + 1]) + pl.chunk_tiles - 1) / pl.chunk_tiles;
+        chunk_begin[tau + 1] = chunk_begin[tau] + (int32_t)n;
+        pl.n_chunks += n;
+    }
+    std::vector<int32_t> win_begin;
+    pl.n_windows = reduce_windows(T, chunk_begin.data(), &win_begin);
     return pl;
 }
 
@@ -117,7 +152,8 @@ void build_plan(int32_t T, const int64_t *off, int32_t chunk_tiles, std::vector<
 }
 
 struct Layout {
-    size_t tiles, chunks, chunk_begin, large, tile_partials, chunk_partials, acc, sched, total;
+    size_t tiles, chunks, chunk_begin, large, tile_partials, chunk_partials, acc, win_begin, win_partials, sched,
+        total;
 };
 
 // A record slot (pinned host memory the reduction writes directly): the
@@ -134,7 +170,9 @@ Layout layout_for(const Plan &pl, int32_t T) {
     l.tile_partials = align_up(l.large + sizeof(int32_t) * (size_t)T, 256);
     l.chunk_partials = align_up(l.tile_partials + 2 * sizeof(double) * at_least_one(pl.n_tiles), 256);
     l.acc = align_up(l.chunk_partials + 2 * sizeof(double) * at_least_one(pl.n_chunks), 256);
-    l.sched = align_up(l.acc + 2 * sizeof(double) * (size_t)T, 256);
+    l.win_begin = align_up(l.acc + 2 * sizeof(double) * (size_t)T, 256);
+    l.win_partials = align_up(l.win_begin + sizeof(int32_t) * (size_t)(pl.n_windows + 1), 256);
+    l.sched = align_up(l.win_partials + 2 * sizeof(double) * at_least_one(pl.n_windows), 256);
     l.total = align_up(l.sched + sizeof(SchedState), 256);
     return l;
 }
@@ -171,6 +209,9 @@ struct adpsgd_ctx {
     std::vector<Chunk> chunks;
     std::vector<int32_t> chunk_begin;
     std::vector<int32_t> large;     // tensors of more than kSmallTensorChunks chunks
+    std::vector<int32_t> win_begin; // windows of tensors for k_reduce_windows (empty: none)
+    int32_t *d_win_begin = nullptr;
+    double *d_win_partials = nullptr;
     adpsgd_hparams hp{};
     adpsgd_buffers buf{};
     hipStream_t stream = nullptr;
@@ -370,6 +411,10 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     r.K = c->K;
     r.large = c->d_large;
     r.n_large = (int32_t)c->large.size();
+    r.win_begin = c->d_win_begin;
+    r.win_partials = c->d_win_partials;
+    r.n_windows = c->win_begin.empty() ? 0 : (int32_t)c->win_begin.size() - 1;
+    r.pad2_ = 0;
     r.hdr = reinterpret_cast<SlotHdr *>(slot_dev(c, slot));
     r.out = reinterpret_cast<double *>(slot_dev(c, slot) + kSlotHdrBytes);
     r.sched = ctl ? c->d_sched : nullptr;
@@ -560,6 +605,12 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->d_chunks = (Chunk *)(ws + lay.chunks);
     c->d_chunk_begin = (int32_t *)(ws + lay.chunk_begin);
     c->d_large = (int32_t *)(ws + lay.large);
+    c->d_win_begin = (int32_t *)(ws + lay.win_begin);
+    c->d_win_partials = (double *)(ws + lay.win_partials);
+    if (reduce_windows(T, c->chunk_begin.data(), &c->win_begin) != plan.n_windows) {
+        release(c);
+        return fail(ADPSGD_EINVAL, "internal: window table disagrees with the workspace plan");
+    }
     for (int32_t tau = 0; tau < T; ++tau)
         if (c->chunk_begin[tau + 1] - c->chunk_begin[tau] > kSmallTensorChunks) c->large.push_back(tau);
     c->d_tile_partials = (double *)(ws + lay.tile_partials);
@@ -602,6 +653,10 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         (e = hipMemcpyAsync(c->d_large, c->large.data(), sizeof(int32_t) * c->large.size(), hipMemcpyHostToDevice,
                             c->stream)) != hipSuccess)
         return bail(e, "copy large-tensor list");
+    if (!c->win_begin.empty() &&
+        (e = hipMemcpyAsync(c->d_win_begin, c->win_begin.data(), sizeof(int32_t) * c->win_begin.size(),
+                            hipMemcpyHostToDevice, c->stream)) != hipSuccess)
+        return bail(e, "copy window table");
     if (P > 0) {
         if ((e = launch_init_problem(buf->h, buf->xstar, P, hp->seed, hp->h_lo, hp->h_hi, c->stream)) != hipSuccess)
             return bail(e, "init_problem launch");

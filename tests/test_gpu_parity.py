@@ -230,6 +230,29 @@ def test_reduction_paths_match_oracle(A, n_tiles, max_size):
     assert max_rel_err(g["m"], r.v, off, floor=MOM_FLOOR) < MOM_TOL
 
 
+def test_reduction_windows_with_large_tensors_match_oracle(A):
+    """More chunk partials than the finishing block's LDS window, with tensors
+    of more than 32 chunks (over 8.4M elements) between runs of small ones:
+    each large tensor is reduced in a window of its own, and a run of small
+    tensors longer than one window is split."""
+    rng = np.random.default_rng(2669)
+    small = lambda n: [int(s) for s in rng.integers(1, 300, size=n)]
+    sizes = tuple(small(1200) + [8_700_001] + small(2500) + [9_000_003] + small(100))
+    w = W.Workload(name="windows_large", K=2, sizes=sizes, seed=2669, sigma=0.1, momentum=0.9,
+                   weight_decay=5e-4, h_lo=1e-2, h_hi=1.0, lr_kind=W.LR_CONST, lr0=0.05,
+                   total_steps=10, period_mode=W.PERIOD_ADAPTIVE, p_init=2, k_s=4)
+    _say(f"reduction windows: T={w.T}, P={w.P}")
+    g = gpu_run(w)
+    r = oracle.Oracle(w).run()
+    recs = g["recs"]
+    assert np.array_equal(recs["t"], r.sync_t) and np.array_equal(recs["p"], r.sync_p)
+    assert rel_err(recs["S"], r.S) < VAR_TOL
+    assert rel_err(g["var"], r.var, floor=1e-300) < VAR_TOL
+    off = w.offsets()
+    assert max_rel_err(g["x"], r.x, off) < PARAM_TOL
+    assert max_rel_err(g["m"], r.v, off, floor=MOM_FLOOR) < MOM_TOL
+
+
 @pytest.mark.parametrize("extra", [1, 2, 3])
 @pytest.mark.parametrize("key", ["resnet18_like", "many_small"])
 def test_padded_and_packed_rows_match_oracle(A, key, extra):
