@@ -126,8 +126,9 @@ typedef struct {
     float *h;               /* [P] curvatures, written by init                               */
     float *xstar;           /* [P] optimum, written by init                                  */
     void *workspace;        /* >= adpsgd_workspace_bytes(...) bytes, 256-byte aligned;
-                               tile and chunk tables, partials, the device copy of the
-                               controller state and the record slots                       */
+                               tile, chunk and window tables, partial sums and the device
+                               copy of the controller state (the records of the reductions
+                               go to pinned host memory that the library allocates)          */
     size_t workspace_bytes;
     void *stream;           /* hipStream_t for every launch and copy; NULL = null stream     */
     int64_t row_stride;     /* elements from one row of x (and of m) to the next, >= P;

@@ -10,16 +10,21 @@
 //                  so a sync costs no extra pass over HBM.
 //   k_sync_loop    the same for a worker count without a compiled variant.
 //   k_reduce_chunks,  fixed-order sums of the tile partials per chunk, then
-//   k_reduce_finish   per tensor and over tensors, and Algorithm 2's period
-//                     decision when a run's schedule lives on the device.
+//   k_reduce_windows  per tensor (in windows of tensors when there are more
+//   k_reduce_finish   chunk partials than one block's LDS holds) and over
+//                     tensors, and Algorithm 2's period decision when a run's
+//                     schedule lives on the device.
+//   k_init_problem, k_zero_rows, k_philox_dump, k_normal_dump: problem data,
+//                  row clearing and the raw generator streams.
 //
 // Work unit: a group of four consecutive elements of one worker's row, moved
 // with one dwordx4 load and store and fed by one Philox call.  On MI355X a
 // stream of one dwordx4 access per thread over a large grid sustains far more
-// HBM bandwidth than threads that each walk many rows, so every thread owns a
-// single (group, worker) pair.  The K threads of a group exchange replicas
-// through LDS at a sync.  No atomics and fixed reduction orders make results
-// bit-reproducible for a given (K, P, offsets).
+// HBM bandwidth than threads that each walk many rows, so every thread of the
+// local step owns a single (group, worker) pair.  At a sync the waves of a
+// tile's block own the K rows and exchange their row sums through LDS.  No
+// atomics and fixed reduction orders make results bit-reproducible for a
+// given (K, P, offsets).
 #include <algorithm>
 #include <cmath>
 

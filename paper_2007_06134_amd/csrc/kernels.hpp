@@ -41,7 +41,7 @@ struct Chunk {
     int32_t pad_;
 };
 
-// Everything a local step needs.  Replicas are rows of x/m with stride P.
+// Everything a local step needs.  Replicas are rows of x and m, ld elements apart.
 struct StepParams {
     float *x;
     float *m;
