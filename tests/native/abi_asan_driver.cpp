@@ -18,7 +18,8 @@ static adpsgd_hparams hp_of(int mode, int p_init, int64_t N, int64_t k_s) {
     return h;
 }
 
-static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t N, int64_t k_s, int policy, bool traced) {
+static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t N, int64_t k_s, int policy, bool traced,
+               bool pad_rows = false) {
     std::vector<int64_t> off(1, 0);
     for (auto s : sizes) off.push_back(off.back() + s);
     const int T = (int)sizes.size();
@@ -27,9 +28,10 @@ static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t 
     size_t ws = adpsgd_workspace_bytes(K, P, T, off.data());
     if (!ws) { printf("workspace 0\n"); return 1; }
     float *x, *m, *h, *xs; void *w;
-    CK(hipMalloc(&x, 4 * (size_t)K * P + 16)); CK(hipMalloc(&m, 4 * (size_t)K * P + 16));
+    const int64_t ld = pad_rows ? (P + 255) / 256 * 256 : P;  // rows 1 KB aligned
+    CK(hipMalloc(&x, 4 * (size_t)K * ld + 16)); CK(hipMalloc(&m, 4 * (size_t)K * ld + 16));
     CK(hipMalloc(&h, 4 * (size_t)P + 16)); CK(hipMalloc(&xs, 4 * (size_t)P + 16)); CK(hipMalloc(&w, ws));
-    adpsgd_buffers b{x, m, h, xs, w, ws, nullptr};
+    adpsgd_buffers b{x, m, h, xs, w, ws, nullptr, pad_rows ? ld : 0};
     adpsgd_ctx *c = nullptr;
     OKC(adpsgd_init(K, P, off.data(), T, &hp, &b, &c));
     OKC(adpsgd_set_launch_policy(c, policy));
@@ -67,21 +69,33 @@ static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t 
     OKC(adpsgd_run(c, 5, nullptr, 0, nullptr, &n));
     OKC(adpsgd_destroy(c));
     CK(hipFree(x)); CK(hipFree(m)); CK(hipFree(h)); CK(hipFree(xs)); CK(hipFree(w));
-    printf("ok K=%d P=%lld T=%d mode=%d policy=%d traced=%d syncs=%lld timed steps=%lld\n", K, (long long)P, T, mode, policy,
-           (int)traced, (long long)n, (long long)tm.step_launches);
+    printf("ok K=%d P=%lld T=%d mode=%d policy=%d traced=%d rows=%s syncs=%lld timed steps=%lld\n", K, (long long)P, T,
+           mode, policy, (int)traced, pad_rows ? "padded" : "packed", (long long)n, (long long)tm.step_launches);
     fflush(stdout);
     return 0;
 }
 
 int main() {
     const std::vector<int64_t> ragged = {5000, 77, 1, 0, 1024, 3, 70000, 263};
+    // more chunk partials than the finishing block's LDS holds: the window
+    // tables (a split run of small tensors and one tensor of over 32 chunks)
+    std::vector<int64_t> many;
+    uint32_t r = 12345;
+    for (int i = 0; i < 3300; ++i) {
+        r = r * 1664525u + 1013904223u;
+        many.push_back(1 + (r >> 8) % 300);
+        if (i == 2500) many.push_back(9000001);
+    }
     for (int policy = 0; policy < 3; ++policy)
         for (int traced = 0; traced < 2; ++traced) {
             if (one(8, ragged, ADPSGD_PERIOD_ADAPTIVE, 1, 120, 30, policy, traced)) return 1;
+            if (one(8, ragged, ADPSGD_PERIOD_ADAPTIVE, 1, 60, 15, policy, traced, true)) return 1;
             if (one(3, ragged, ADPSGD_PERIOD_ADAPTIVE, 2, 90, 20, policy, traced)) return 1;
             if (one(32, {300000}, ADPSGD_PERIOD_CONST, 4, 40, 0, policy, traced)) return 1;
             if (one(4, {0, 0}, ADPSGD_PERIOD_ALG1, 3, 20, 0, policy, traced)) return 1;
+            if (one(2, many, ADPSGD_PERIOD_ADAPTIVE, 2, 24, 6, policy, traced)) return 1;
         }
     printf("all ok\n");
+    fflush(stdout);
     return 0;
 }

@@ -2,7 +2,10 @@
 # Builds tests/native/abi_asan_driver: the library's sources and the driver
 # with AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (each -fsanitize follows
 # -Xarch_host; the GPU code is not instrumented).  Run the result on a GPU with
-# ASAN_OPTIONS=detect_leaks=0 (the HIP runtime keeps allocations until exit).
+# ASAN_OPTIONS=detect_leaks=0:quarantine_size_mb=4096: the HIP runtime keeps
+# allocations until exit, and a quarantine larger than all the device memory
+# the driver frees (about 2 GB) keeps ASan from recycling freed device chunks
+# while the runtime unloads at exit, which fails one of ASan's own checks.
 set -e
 HERE=$(cd "$(dirname "$0")" && pwd)
 ROOT=$(cd "$HERE/../.." && pwd)
