@@ -421,23 +421,54 @@ __device__ __forceinline__ bool reduce_due(const ReduceParams &r, int32_t *p_t, 
     return sync_due(r.rule, st->cnt + (r.t - st->t) + 1, *p_t, r.t);
 }
 
-// Level 1, one block per chunk: the chunk's tile partials, summed in a fixed
-// order (strided per thread, then the block tree).
+// Level 1, one wave per chunk (kChunksPerBlock chunks per block): the chunk's
+// tile partials, summed in a fixed order (strided over the lanes, then a
+// butterfly).  A chunk holds at most kChunkTiles = 1024 tiles, 16 per lane;
+// problems of thousands of small tensors have as many one-tile chunks, which
+// would otherwise cost a block each.
+constexpr int kChunksPerBlock = kBlock / 64;
 __global__ void __launch_bounds__(kBlock) k_reduce_chunks(ReduceParams r) {
     int32_t p_t;
     SchedState st;
     if (!reduce_due(r, &p_t, &st) && !r.traced) return;
-    const int64_t ci = (int64_t)r.block0 + blockIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int64_t ci = ((int64_t)r.block0 + blockIdx.x) * kChunksPerBlock + (threadIdx.x >> 6);
+    if (ci >= r.n_chunks) return;  // whole waves: no block-wide barrier follows
     const Chunk c = r.chunks[ci];
     double a = 0.0, b = 0.0;
-    for (int32_t i = (int32_t)threadIdx.x; i < c.count; i += kBlock) {
-        a += r.tile_partials[2 * (int64_t)(c.first + i)];
-        b += r.tile_partials[2 * (int64_t)(c.first + i) + 1];
+    if (c.count <= 64) {  // uniform over the wave: one tile partial per lane at most
+        if (lane < c.count) {
+            a = r.tile_partials[2 * (int64_t)(c.first + lane)];
+            b = r.tile_partials[2 * (int64_t)(c.first + lane) + 1];
+        }
+    } else {
+        // all of a lane's loads are issued before the first add; the sum is
+        // then taken in lane-stride order (the zeros of lanes past the chunk
+        // leave it unchanged, so both branches give the same bits)
+        constexpr int kPerLane = kChunkTiles / 64;
+        static_assert(kPerLane * 64 == kChunkTiles, "chunk tiles per lane");
+        double va[kPerLane], vb[kPerLane];
+#pragma unroll
+        for (int j = 0; j < kPerLane; ++j) {
+            const int32_t i = lane + 64 * j;
+            const bool in_chunk = i < c.count;
+            va[j] = in_chunk ? r.tile_partials[2 * (int64_t)(c.first + i)] : 0.0;
+            vb[j] = in_chunk ? r.tile_partials[2 * (int64_t)(c.first + i) + 1] : 0.0;
+        }
+#pragma unroll
+        for (int j = 0; j < kPerLane; ++j) {
+            a += va[j];
+            b += vb[j];
+        }
     }
-    const Pair cs = block_sum2<kBlock / 64>(a, b);
-    if (threadIdx.x == 0) {
-        r.chunk_partials[2 * ci] = cs.a;
-        r.chunk_partials[2 * ci + 1] = cs.b;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+    }
+    if (lane == 0) {
+        r.chunk_partials[2 * ci] = a;
+        r.chunk_partials[2 * ci + 1] = b;
     }
 }
 
@@ -828,7 +859,8 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
 
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {
     if (r.n_chunks > 0 && !r.chunks_are_tiles) {
-        const hipError_t e = in_pieces(r.n_chunks, kBlock, [&](int64_t b0, unsigned nb) {
+        const int64_t blocks = (r.n_chunks + kChunksPerBlock - 1) / kChunksPerBlock;
+        const hipError_t e = in_pieces(blocks, kBlock, [&](int64_t b0, unsigned nb) {
             ReduceParams q = r;
             q.block0 = (int32_t)b0;
             k_reduce_chunks<<<dim3(nb), dim3(kBlock), 0, st>>>(q);

@@ -136,7 +136,7 @@ struct ReduceParams {
     const int32_t *large;         // [n_large] tensors of more than kSmallTensorChunks chunks
     int32_t n_chunks, T, K, n_large;
     int32_t chunks_are_tiles;     // 1: chunk_partials is tile_partials (one tile per chunk)
-    int32_t block0;               // first chunk of this launch of the chunk sums (set by launch_reduce)
+    int32_t block0;               // first block of this launch of the chunk sums (set by launch_reduce)
     // More chunk partials than one LDS window: the tensors are cut into
     // windows (a run of whole small tensors whose chunks fit one window, or one
     // large tensor), reduced by one block each; the finishing block then sums
