@@ -8,7 +8,9 @@
 //                  (the parameter variance of Section II-B), broadcast of the
 //                  mean; optionally fused behind the period's last local step
 //                  so a sync costs no extra pass over HBM.
-//   k_sync_loop    the same for a worker count without a compiled variant.
+//   k_sync_loop    the same for odd K above 15 and K above 32 (other K take
+//                  k_sync_lds, compiled for powers of two or with K as an
+//                  argument).
 //   k_reduce_chunks,  fixed-order sums of the tile partials per chunk, then
 //   k_reduce_windows  per tensor (in windows of tensors when there are more
 //   k_reduce_finish   chunk partials than one block's LDS holds) and over
@@ -199,6 +201,28 @@ __device__ __forceinline__ f4 tree_sum_regs(const f4 *v, int base) {
     }
 }
 
+// The replica mean at one lane from the W wave sums in LDS: the pairwise tree
+// of a compiled K (WC = W waves), else the sums in wave order.
+template <int KT, int WC>
+__device__ __forceinline__ f4 lds_mean(const f4 (*rows)[64], int lane, int W, int K) {
+    if constexpr (KT > 0) {
+        return tree_sum_lds<WC>(rows, lane, 0) / splat((float)KT);
+    } else {
+        // the reads go out four at a time, and the adds run in wave order
+        f4 s = rows[0][lane];
+#pragma unroll 1
+        for (int w0 = 1; w0 < W; w0 += 4) {
+            f4 v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = w0 + j < W ? rows[w0 + j][lane] : splat(0.0f);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (w0 + j < W) s = s + v[j];
+        }
+        return s / splat((float)K);
+    }
+}
+
 // Step s.t of a run whose schedule lives on the device: does a sync follow
 // it?  Every thread reads the same state (written only by the reduction
 // kernel after a sync), so the answer is uniform over the launch.
@@ -222,21 +246,51 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 // use masked scalar accesses.
 // Waves per block: one per worker row (at most 16) when the rows are stepped;
 // the averaging-only mode does best with two rows per wave (measured +2 to +15%).
+// KT = 0: K is a kernel argument (a K without a compiled variant: an even
+// K <= 32 with RD = 2 rows per wave, or an odd K <= 15 with RD = 1, in every
+// mode alike);
+// the W = K / RD wave sums are then added in wave order, and the mean of equal
+// replicas need not be exact.
 template <int KT, int MODE>
 constexpr int sync_waves() {
-    if constexpr (MODE == kAverage && KT >= 2) return KT / 2 < 16 ? KT / 2 : 16;
+    if constexpr (KT == 0) return 16;  // the most waves a block of the K-argument kernel has
+    else if constexpr (MODE == kAverage && KT >= 2) return KT / 2 < 16 ? KT / 2 : 16;
     else return KT < 16 ? KT : 16;
 }
 
-template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
+// block_sum2 over a run-time number of waves (at most 16), in the same order.
+__device__ __forceinline__ Pair block_sum2_waves(double a, double b, int waves) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        a += __shfl_xor(a, off, 64);
+        b += __shfl_xor(b, off, 64);
+    }
+    __shared__ double wave_a[16], wave_b[16];
+    if ((threadIdx.x & 63) == 0) {
+        wave_a[threadIdx.x >> 6] = a;
+        wave_b[threadIdx.x >> 6] = b;
+    }
+    __syncthreads();
+    Pair total{0.0, 0.0};
+    if (threadIdx.x == 0)
+        for (int w = 0; w < waves; ++w) {
+            total.a += wave_a[w];
+            total.b += wave_b[w];
+        }
+    return total;
+}
+
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD = 0>
 __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(SyncParams p) {
-    constexpr int W = sync_waves<KT, MODE>();
-    constexpr int R = KT / W;
+    static_assert((KT == 0) == (RD > 0), "RD (rows per wave) is given exactly when K is an argument");
+    constexpr int WMAX = sync_waves<KT, MODE>();
+    constexpr int R = KT > 0 ? KT / WMAX : RD;
+    const int W = KT > 0 ? WMAX : p.s.K / (RD > 0 ? RD : 1);
     constexpr bool STEP = MODE != kAverage;
     constexpr bool GN = MODE == kDeviceTrace;
     // wave w owns rows R w .. R w + R - 1 and publishes their subtree sum
-    __shared__ f4 part[W][64];
-    __shared__ f4 mpart[AVGM ? W : 1][64];
+    __shared__ f4 part[WMAX][64];
+    __shared__ f4 mpart[AVGM ? WMAX : 1][64];
     const StepParams &a = p.s;
     bool bcast = true;  // the host-decided modes always average
     if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
@@ -291,7 +345,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     __syncthreads();
     double acc = 0.0, gn = 0.0;
     if (active) {
-        const f4 mean = tree_sum_lds<W>(part, lane, 0) / splat((float)KT);
+        const f4 mean = lds_mean<KT, WMAX>(part, lane, W, a.K);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             // squared deviations in fp32 per element, each row's sum in fp64
@@ -305,7 +359,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (avg_m) {
-            const f4 mmean = tree_sum_lds<W>(mpart, lane, 0) / splat((float)KT);
+            const f4 mmean = lds_mean<KT, WMAX>(mpart, lane, W, a.K);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 float *mrow = a.m + (int64_t)(R * w + r) * a.ld + e0;
@@ -314,7 +368,9 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         }
         if (GN && w == 0) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
-    const Pair total = block_sum2<W>(acc, gn);
+    Pair total;
+    if constexpr (KT > 0) total = block_sum2<WMAX>(acc, gn);
+    else total = block_sum2_waves(acc, gn, W);
     if (threadIdx.x == 0) {
         p.partials[2 * ti] = total.a;
         p.partials[2 * ti + 1] = total.b;
@@ -740,37 +796,43 @@ size_t static_lds_of(Kern kern) {
     return hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kern)) == hipSuccess ? fa.sharedSizeBytes : 0;
 }
 
-template <int KT, bool VEC, bool NT, int MODE, bool AVGM>
+// Rows per wave of the K-argument sync-tile kernel for K (0: no such kernel;
+// the loop kernel takes K).  Two rows per wave whenever K is even: a CU holds
+// at most two blocks of 9-16 waves, and two rows per wave keep twice the
+// bytes in flight.
+constexpr int any_k_rows(int K) { return K <= 32 && K % 2 == 0 ? 2 : (K <= 16 ? 1 : 0); }
+
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD>
 hipError_t sync_variant(const SyncParams &p, int64_t n_tiles, int cap, hipStream_t st) {
-    constexpr int threads = 64 * sync_waves<KT, MODE>();
-    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM>);
+    const int threads = KT > 0 ? 64 * sync_waves<KT, MODE>() : 64 * (p.s.K / RD);
+    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD>);
     const int lds = cap_lds(cap, own);
     return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
         SyncParams q = p;
         q.s.block0 = b0;
-        k_sync_lds<KT, VEC, NT, MODE, AVGM><<<dim3(nb), dim3(threads), lds, st>>>(q);
+        k_sync_lds<KT, VEC, NT, MODE, AVGM, RD><<<dim3(nb), dim3(threads), lds, st>>>(q);
     });
 }
 
-template <int KT, int MODE, bool AVGM>
+template <int KT, int MODE, bool AVGM, int RD>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, int cap, hipStream_t st) {
-    if (vec && nt) return sync_variant<KT, true, true, MODE, AVGM>(p, n_tiles, cap, st);
-    if (vec) return sync_variant<KT, true, false, MODE, AVGM>(p, n_tiles, cap, st);
-    return sync_variant<KT, false, false, MODE, AVGM>(p, n_tiles, cap, st);
+    if (vec && nt) return sync_variant<KT, true, true, MODE, AVGM, RD>(p, n_tiles, cap, st);
+    if (vec) return sync_variant<KT, true, false, MODE, AVGM, RD>(p, n_tiles, cap, st);
+    return sync_variant<KT, false, false, MODE, AVGM, RD>(p, n_tiles, cap, st);
 }
 
-template <int KT>
+template <int KT, int RD = 0>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt, int cap,
                          hipStream_t st) {
     switch (mode) {
-    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true>(p, n_tiles, vec, nt, cap, st)
-                                : sync_dispatch<KT, kAverage, false>(p, n_tiles, vec, nt, cap, st);
-    case kFused: return avg_m ? sync_dispatch<KT, kFused, true>(p, n_tiles, vec, nt, cap, st)
-                              : sync_dispatch<KT, kFused, false>(p, n_tiles, vec, nt, cap, st);
-    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true>(p, n_tiles, vec, nt, cap, st)
-                               : sync_dispatch<KT, kDevice, false>(p, n_tiles, vec, nt, cap, st);
-    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true>(p, n_tiles, vec, nt, cap, st)
-                          : sync_dispatch<KT, kDeviceTrace, false>(p, n_tiles, vec, nt, cap, st);
+    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true, RD>(p, n_tiles, vec, nt, cap, st)
+                                : sync_dispatch<KT, kAverage, false, RD>(p, n_tiles, vec, nt, cap, st);
+    case kFused: return avg_m ? sync_dispatch<KT, kFused, true, RD>(p, n_tiles, vec, nt, cap, st)
+                              : sync_dispatch<KT, kFused, false, RD>(p, n_tiles, vec, nt, cap, st);
+    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true, RD>(p, n_tiles, vec, nt, cap, st)
+                               : sync_dispatch<KT, kDevice, false, RD>(p, n_tiles, vec, nt, cap, st);
+    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true, RD>(p, n_tiles, vec, nt, cap, st)
+                          : sync_dispatch<KT, kDeviceTrace, false, RD>(p, n_tiles, vec, nt, cap, st);
     }
 }
 
@@ -839,7 +901,7 @@ int sync_tile_waves(int K, int mode) {
     case 8: return avg ? sync_waves<8, kAverage>() : sync_waves<8, kFused>();
     case 16: return avg ? sync_waves<16, kAverage>() : sync_waves<16, kFused>();
     case 32: return avg ? sync_waves<32, kAverage>() : sync_waves<32, kFused>();
-    default: return 0;
+    default: return K > 0 && any_k_rows(K) > 0 ? K / any_k_rows(K) : 0;
     }
 }
 
@@ -853,7 +915,10 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
     case 8: return sync_dispatch<8>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
     case 16: return sync_dispatch<16>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
     case 32: return sync_dispatch<32>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
-    default: return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
+    default:
+        if (p.s.K > 0 && any_k_rows(p.s.K) == 1) return sync_dispatch<0, 1>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        if (p.s.K > 0 && any_k_rows(p.s.K) == 2) return sync_dispatch<0, 2>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
     }
 }
 

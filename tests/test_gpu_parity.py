@@ -92,7 +92,7 @@ def test_problem_data_matches_oracle(A, P):
 
 # ---------------------------------------------------------------- local steps and sync
 
-@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 16, 32])
+@pytest.mark.parametrize("K", [1, 2, 3, 4, 8, 12, 16, 24, 32])
 @pytest.mark.parametrize("sizes", [(4096 * 3 + 4,), (5000, 3, 5001, 993)])   # aligned / ragged P
 def test_local_steps_match_oracle(A, K, sizes):
     w = _tiny(K=K, sizes=sizes)
@@ -109,7 +109,9 @@ def test_local_steps_match_oracle(A, K, sizes):
     assert max_rel_err(m, r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
 
 
-@pytest.mark.parametrize("K", [1, 3, 8, 32])
+# K = 3, 12: the sync-tile kernel with K as an argument (a row per wave); 24:
+# the same with two rows per wave; 33: the loop kernel
+@pytest.mark.parametrize("K", [1, 3, 8, 12, 24, 32, 33])
 @pytest.mark.parametrize("sizes", [(4096 * 3 + 4,), (5000, 3, 0, 5001, 993, 1), (8192, 4096, 12)])
 def test_average_matches_oracle(A, K, sizes):
     w = _tiny(K=K, sizes=sizes)
@@ -135,22 +137,23 @@ def test_average_matches_oracle(A, K, sizes):
     assert rel_err(var[~empty], var_o[~empty]) < VAR_TOL
 
 
-@pytest.mark.parametrize("K", [2, 5, 8, 32])
+@pytest.mark.parametrize("K", [2, 3, 5, 8, 12, 24, 32, 33])
 def test_fused_sync_equals_step_then_sync(A, K):
     w = _tiny(K=K, sizes=(4099, 1, 8000, 6))
     _say(f"fused vs separate K={K}")
     with A.Adpsgd.from_workload(w) as a, A.Adpsgd.from_workload(w) as b:
         a.local_steps(4); va = a.step_average()
         b.local_steps(5); vb = b.average()
-        # the replicas are bitwise equal (the same mean tree); the separate sync
-        # gives each wave two rows, so its variance sums round in another order
+        # the replicas are bitwise equal (the same order of the mean); for a
+        # compiled K the separate sync gives each wave two rows, so its
+        # variance sums round in another order
         assert np.allclose(va, vb, rtol=1e-12, atol=0.0)
         assert a.get_state().t == b.get_state().t == 5
         import torch
         assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
 
 
-@pytest.mark.parametrize("K", [3, 8, 32])
+@pytest.mark.parametrize("K", [3, 8, 12, 24, 32, 33])
 def test_second_sync_has_zero_variance(A, K):
     w = _tiny(K=K, sizes=(3000, 5000))
     with A.Adpsgd.from_workload(w) as eng:
@@ -294,13 +297,13 @@ def test_runs_are_bit_reproducible(A):
     assert np.array_equal(a["var"], b["var"]) and a["recs"].tobytes() == b["recs"].tobytes()
 
 
-@pytest.mark.parametrize("key", ["resnet18_like", "many_small", "vgg16_adaptive", "k3_adaptive"])
+@pytest.mark.parametrize("key", ["resnet18_like", "many_small", "vgg16_adaptive", "k3_adaptive", "k24_adaptive"])
 def test_launch_policies_agree_bitwise(A, key):
     """Host-planned, device-decided and host-waiting launches give the same bits:
     every step runs the same update code and every sync the same reduction and
     controller, whichever kernel the driver chose for it."""
-    if key == "k3_adaptive":
-        w = _tiny(K=3, sizes=(5000, 77, 1024, 3), p_init=2, total_steps=120,
+    if key in ("k3_adaptive", "k24_adaptive"):
+        w = _tiny(K=int(key[1:key.index("_")]), sizes=(5000, 77, 1024, 3), p_init=2, total_steps=120,
                   period_mode=W.PERIOD_ADAPTIVE, k_s=30)
     else:
         w = W.parity_workloads()[key]
@@ -723,12 +726,14 @@ def _variant(name):
                                 p_init=5, k_s=0),
         "avg_momentum_k32": dict(K=32, total_steps=200, avg_momentum=True, period_mode=W.PERIOD_CONST,
                                  p_init=3, k_s=0),
+        "avg_momentum_k24": dict(K=24, total_steps=200, avg_momentum=True, k_s=50),
     }[name]
     return base.replace(name=name, **v)
 
 
 @pytest.mark.parametrize("name", ["imagenet_warmup", "alg1", "two_phase_up", "two_phase_down",
-                                  "avg_momentum_adaptive", "avg_momentum_k3", "avg_momentum_k32"])
+                                  "avg_momentum_adaptive", "avg_momentum_k3", "avg_momentum_k32",
+                                  "avg_momentum_k24"])
 def test_variant_run_matches_oracle(A, name):
     w = _variant(name)
     _say(f"variant {name}: K={w.K} P={w.P} N={w.total_steps}")
@@ -748,7 +753,7 @@ def test_variant_run_matches_oracle(A, name):
         assert all(np.array_equal(m[k], m[0]) for k in range(w.K))   # synced at the last step
 
 
-@pytest.mark.parametrize("K", [3, 8, 32])
+@pytest.mark.parametrize("K", [3, 8, 12, 24, 32, 33])
 def test_separate_sync_averages_momentum(A, K):
     w = _tiny(K=K, sizes=(5000, 3, 0, 5001), avg_momentum=True)
     with A.Adpsgd.from_workload(w) as eng:
@@ -775,6 +780,8 @@ def _traced_cases():
         "resnet18_like": pw["resnet18_like"].replace(total_steps=1200, k_s=300),
         "many_small": pw["many_small"].replace(total_steps=800, k_s=200),
         "k3_const": _tiny(K=3, sizes=(5000, 3, 0, 5001), p_init=5, total_steps=60),
+        "k24_adaptive": _tiny(K=24, sizes=(5000, 3, 0, 5001), p_init=2, total_steps=80,
+                              period_mode=W.PERIOD_ADAPTIVE, k_s=20),
         "vgg16_adaptive": pw["vgg16_adaptive"],
     }
 
