@@ -8,9 +8,9 @@
 //                  (the parameter variance of Section II-B), broadcast of the
 //                  mean; optionally fused behind the period's last local step
 //                  so a sync costs no extra pass over HBM.
-//   k_sync_loop    the same for odd K above 15, K above 32 and the separate
-//                  sync at K = 3 (other K take k_sync_lds, compiled for powers
-//                  of two or with K as an argument).
+//   k_sync_loop    the same for K above 32 and the separate sync at K = 3
+//                  (other K take k_sync_lds, compiled for powers of two or
+//                  with K as an argument).
 //   k_reduce_chunks,  fixed-order sums of the tile partials per chunk, then
 //   k_reduce_windows  per tensor (in windows of tensors when there are more
 //   k_reduce_finish   chunk partials than one block's LDS holds) and over
@@ -246,10 +246,9 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 // use masked scalar accesses.
 // Waves per block: one per worker row (at most 16) when the rows are stepped;
 // the averaging-only mode does best with two rows per wave (measured +2 to +15%).
-// KT = 0: K is a kernel argument (a K without a compiled variant: an even
-// K <= 32 or an odd K <= 15, with RD = 2 rows per wave, or K = 3 with one);
-// the K / 2 pair sums of an even K, or the K rows of an odd K, are then added
-// in order, and the mean of equal replicas need not be exact.
+// KT = 0: K is a kernel argument (a K up to 32 without a compiled variant,
+// with RD = 2 rows per wave, or K = 3 with one); the W wave sums are then
+// added in wave order, and the mean of equal replicas need not be exact.
 template <int KT, int MODE>
 constexpr int sync_waves() {
     if constexpr (KT == 0) return 16;  // the most waves a block of the K-argument kernel has
@@ -279,20 +278,18 @@ __device__ __forceinline__ Pair block_sum2_waves(double a, double b, int waves) 
     return total;
 }
 
-// ALONE (K an argument, odd K): each wave holds two rows but publishes each
-// row in LDS on its own, so the mean adds the K rows in row order, as one row
-// per wave would; the last wave's second row does not exist.
-template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD = 0, bool ALONE = false>
+// RAGGED (K an argument, odd K, two rows per wave): the last wave holds one
+// row and publishes it alone; the mean adds the (K + 1) / 2 entries in order.
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD = 0, bool RAGGED = false>
 __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(SyncParams p) {
     static_assert((KT == 0) == (RD > 0), "RD (rows per wave) is given exactly when K is an argument");
-    static_assert(!ALONE || RD == 2, "rows published alone come two to a wave");
+    static_assert(!RAGGED || RD == 2, "a ragged last wave comes with two rows per wave");
     constexpr int WMAX = sync_waves<KT, MODE>();
     constexpr int R = KT > 0 ? KT / WMAX : RD;
-    const int W = KT > 0 ? WMAX : (ALONE ? (p.s.K + 1) / 2 : p.s.K / (RD > 0 ? RD : 1));
+    const int W = KT > 0 ? WMAX : (p.s.K + (RD > 0 ? RD : 1) - 1) / (RD > 0 ? RD : 1);
     constexpr bool STEP = MODE != kAverage;
     constexpr bool GN = MODE == kDeviceTrace;
-    // wave w owns rows R w .. R w + R - 1 and publishes their subtree sum (or,
-    // ALONE, each of them; WMAX = 16 rows hold every odd K up to 15)
+    // wave w owns rows R w .. R w + R - 1 and publishes their subtree sum
     __shared__ f4 part[WMAX][64];
     __shared__ f4 mpart[AVGM ? WMAX : 1][64];
     const StepParams &a = p.s;
@@ -311,7 +308,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     // row R w + r exists (only the last wave's second row can be missing)
     bool has[R];
 #pragma unroll
-    for (int r = 0; r < R; ++r) has[r] = !ALONE || R * w + r < a.K;
+    for (int r = 0; r < R; ++r) has[r] = !RAGGED || R * w + r < a.K;
     f4 xr[R];
     f4 h = splat(0.0f), xs = splat(0.0f);
     if (active) {
@@ -349,13 +346,9 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (measure) {
-            if constexpr (ALONE) {
-#pragma unroll
-                for (int r = 0; r < R; ++r)
-                    if (has[r]) {
-                        part[R * w + r][lane] = xr[r];
-                        if (AVGM) mpart[R * w + r][lane] = m[r];
-                    }
+            if (RAGGED && !has[R - 1]) {  // the last wave of an odd K: one row
+                part[w][lane] = xr[0];
+                if (AVGM) mpart[w][lane] = m[0];
             } else {
                 part[w][lane] = tree_sum_regs<R>(xr, 0);
                 if (AVGM) mpart[w][lane] = tree_sum_regs<R>(m, 0);
@@ -366,8 +359,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     __syncthreads();
     double acc = 0.0, gn = 0.0;
     if (active) {
-        const int n_lds = ALONE ? a.K : W;  // LDS entries the mean adds
-        const f4 mean = lds_mean<KT, WMAX>(part, lane, n_lds, a.K);
+        const f4 mean = lds_mean<KT, WMAX>(part, lane, W, a.K);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             if (!has[r]) continue;
@@ -382,7 +374,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (avg_m) {
-            const f4 mmean = lds_mean<KT, WMAX>(mpart, lane, n_lds, a.K);
+            const f4 mmean = lds_mean<KT, WMAX>(mpart, lane, W, a.K);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 if (!has[r]) continue;
@@ -821,51 +813,50 @@ size_t static_lds_of(Kern kern) {
 }
 
 // Does the K-argument sync-tile kernel take K in this mode (else the loop
-// kernel does)?  Two rows per wave: a CU holds at most two blocks of 9-16
-// waves, and two rows per wave keep twice the bytes in flight.  An even K
-// publishes row pairs, an odd K (up to 15, so the rows fit 16 LDS entries)
-// each row alone.  K = 3 is the exception: one row per wave in the modes with
-// a step, and the loop kernel for the separate sync (76% of peak, against 58%
-// and 48% for three one-row or two two-row waves); all three add the rows in
-// row order, so the replicas keep the same bits.
+// kernel does)?  Two rows per wave (K up to 32; the last wave of an odd K
+// holds one): a CU holds at most two blocks of 9-16 waves, and two rows per
+// wave keep twice the bytes in flight.  K = 3 is the exception: one row per
+// wave in the modes with a step, and the loop kernel for the separate sync
+// (76% of peak, against 58% and 48% for three one-row or two two-row waves);
+// both add the rows in row order, so the replicas keep the same bits.
 constexpr bool any_k_kernel(int K, int mode) {
     if (K == 3) return mode != kAverage;
-    return K > 0 && (K % 2 == 0 ? K <= 32 : K <= 15);
+    return K > 0 && K <= 32;
 }
 constexpr int any_k_rows(int K) { return K == 3 ? 1 : 2; }
 constexpr int any_k_waves(int K) { return (K + any_k_rows(K) - 1) / any_k_rows(K); }
 
-template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD, bool ALONE>
+template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD, bool RAGGED>
 hipError_t sync_variant(const SyncParams &p, int64_t n_tiles, int cap, hipStream_t st) {
     const int threads = KT > 0 ? 64 * sync_waves<KT, MODE>() : 64 * any_k_waves(p.s.K);
-    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, ALONE>);
+    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED>);
     const int lds = cap_lds(cap, own);
     return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
         SyncParams q = p;
         q.s.block0 = b0;
-        k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, ALONE><<<dim3(nb), dim3(threads), lds, st>>>(q);
+        k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED><<<dim3(nb), dim3(threads), lds, st>>>(q);
     });
 }
 
-template <int KT, int MODE, bool AVGM, int RD, bool ALONE>
+template <int KT, int MODE, bool AVGM, int RD, bool RAGGED>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, bool vec, bool nt, int cap, hipStream_t st) {
-    if (vec && nt) return sync_variant<KT, true, true, MODE, AVGM, RD, ALONE>(p, n_tiles, cap, st);
-    if (vec) return sync_variant<KT, true, false, MODE, AVGM, RD, ALONE>(p, n_tiles, cap, st);
-    return sync_variant<KT, false, false, MODE, AVGM, RD, ALONE>(p, n_tiles, cap, st);
+    if (vec && nt) return sync_variant<KT, true, true, MODE, AVGM, RD, RAGGED>(p, n_tiles, cap, st);
+    if (vec) return sync_variant<KT, true, false, MODE, AVGM, RD, RAGGED>(p, n_tiles, cap, st);
+    return sync_variant<KT, false, false, MODE, AVGM, RD, RAGGED>(p, n_tiles, cap, st);
 }
 
-template <int KT, int RD = 0, bool ALONE = false>
+template <int KT, int RD = 0, bool RAGGED = false>
 hipError_t sync_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec, bool nt, int cap,
                          hipStream_t st) {
     switch (mode) {
-    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true, RD, ALONE>(p, n_tiles, vec, nt, cap, st)
-                                : sync_dispatch<KT, kAverage, false, RD, ALONE>(p, n_tiles, vec, nt, cap, st);
-    case kFused: return avg_m ? sync_dispatch<KT, kFused, true, RD, ALONE>(p, n_tiles, vec, nt, cap, st)
-                              : sync_dispatch<KT, kFused, false, RD, ALONE>(p, n_tiles, vec, nt, cap, st);
-    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true, RD, ALONE>(p, n_tiles, vec, nt, cap, st)
-                               : sync_dispatch<KT, kDevice, false, RD, ALONE>(p, n_tiles, vec, nt, cap, st);
-    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true, RD, ALONE>(p, n_tiles, vec, nt, cap, st)
-                          : sync_dispatch<KT, kDeviceTrace, false, RD, ALONE>(p, n_tiles, vec, nt, cap, st);
+    case kAverage: return avg_m ? sync_dispatch<KT, kAverage, true, RD, RAGGED>(p, n_tiles, vec, nt, cap, st)
+                                : sync_dispatch<KT, kAverage, false, RD, RAGGED>(p, n_tiles, vec, nt, cap, st);
+    case kFused: return avg_m ? sync_dispatch<KT, kFused, true, RD, RAGGED>(p, n_tiles, vec, nt, cap, st)
+                              : sync_dispatch<KT, kFused, false, RD, RAGGED>(p, n_tiles, vec, nt, cap, st);
+    case kDevice: return avg_m ? sync_dispatch<KT, kDevice, true, RD, RAGGED>(p, n_tiles, vec, nt, cap, st)
+                               : sync_dispatch<KT, kDevice, false, RD, RAGGED>(p, n_tiles, vec, nt, cap, st);
+    default: return avg_m ? sync_dispatch<KT, kDeviceTrace, true, RD, RAGGED>(p, n_tiles, vec, nt, cap, st)
+                          : sync_dispatch<KT, kDeviceTrace, false, RD, RAGGED>(p, n_tiles, vec, nt, cap, st);
     }
 }
 
@@ -952,7 +943,7 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
         if (!any_k_kernel(p.s.K, mode)) return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
         if (any_k_rows(p.s.K) == 1) return sync_dispatch<0, 1, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
         if (p.s.K % 2 == 0) return sync_dispatch<0, 2, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
-        return sync_dispatch<0, 2, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        return sync_dispatch<0, 2, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);  // odd K, ragged
     }
 }
 

@@ -109,9 +109,10 @@ def test_local_steps_match_oracle(A, K, sizes):
     assert max_rel_err(m, r.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
 
 
-# K = 3, 12: the sync-tile kernel with K as an argument (a row per wave); 24:
-# the same with two rows per wave; 33: the loop kernel
-@pytest.mark.parametrize("K", [1, 3, 8, 12, 24, 32, 33])
+# K = 12, 24: the sync-tile kernel with K as an argument (two rows per wave);
+# 25: the same with a ragged last wave; 3: the loop kernel for the separate
+# sync (one row per wave when a step comes first); 33: the loop kernel
+@pytest.mark.parametrize("K", [1, 3, 8, 12, 24, 25, 32, 33])
 @pytest.mark.parametrize("sizes", [(4096 * 3 + 4,), (5000, 3, 0, 5001, 993, 1), (8192, 4096, 12)])
 def test_average_matches_oracle(A, K, sizes):
     w = _tiny(K=K, sizes=sizes)
@@ -137,7 +138,7 @@ def test_average_matches_oracle(A, K, sizes):
     assert rel_err(var[~empty], var_o[~empty]) < VAR_TOL
 
 
-@pytest.mark.parametrize("K", [2, 3, 5, 8, 12, 24, 32, 33])
+@pytest.mark.parametrize("K", [2, 3, 5, 8, 12, 24, 25, 32, 33])
 def test_fused_sync_equals_step_then_sync(A, K):
     w = _tiny(K=K, sizes=(4099, 1, 8000, 6))
     _say(f"fused vs separate K={K}")
@@ -153,7 +154,7 @@ def test_fused_sync_equals_step_then_sync(A, K):
         assert torch.equal(a.x, b.x) and torch.equal(a.m, b.m)
 
 
-@pytest.mark.parametrize("K", [3, 8, 12, 24, 32, 33])
+@pytest.mark.parametrize("K", [3, 8, 12, 24, 25, 32, 33])
 def test_second_sync_has_zero_variance(A, K):
     w = _tiny(K=K, sizes=(3000, 5000))
     with A.Adpsgd.from_workload(w) as eng:
@@ -297,12 +298,13 @@ def test_runs_are_bit_reproducible(A):
     assert np.array_equal(a["var"], b["var"]) and a["recs"].tobytes() == b["recs"].tobytes()
 
 
-@pytest.mark.parametrize("key", ["resnet18_like", "many_small", "vgg16_adaptive", "k3_adaptive", "k24_adaptive"])
+@pytest.mark.parametrize("key", ["resnet18_like", "many_small", "vgg16_adaptive", "k3_adaptive", "k24_adaptive",
+                                 "k25_adaptive"])
 def test_launch_policies_agree_bitwise(A, key):
     """Host-planned, device-decided and host-waiting launches give the same bits:
     every step runs the same update code and every sync the same reduction and
     controller, whichever kernel the driver chose for it."""
-    if key in ("k3_adaptive", "k24_adaptive"):
+    if key in ("k3_adaptive", "k24_adaptive", "k25_adaptive"):
         w = _tiny(K=int(key[1:key.index("_")]), sizes=(5000, 77, 1024, 3), p_init=2, total_steps=120,
                   period_mode=W.PERIOD_ADAPTIVE, k_s=30)
     else:
@@ -753,7 +755,7 @@ def test_variant_run_matches_oracle(A, name):
         assert all(np.array_equal(m[k], m[0]) for k in range(w.K))   # synced at the last step
 
 
-@pytest.mark.parametrize("K", [3, 8, 12, 24, 32, 33])
+@pytest.mark.parametrize("K", [3, 5, 8, 12, 24, 25, 32, 33])
 def test_separate_sync_averages_momentum(A, K):
     w = _tiny(K=K, sizes=(5000, 3, 0, 5001), avg_momentum=True)
     with A.Adpsgd.from_workload(w) as eng:
