@@ -8,9 +8,9 @@
 //                  (the parameter variance of Section II-B), broadcast of the
 //                  mean; optionally fused behind the period's last local step
 //                  so a sync costs no extra pass over HBM.
-//   k_sync_loop    the same for K above 32 and the separate sync at K = 3
-//                  (other K take k_sync_lds, compiled for powers of two or
-//                  with K as an argument).
+//   k_sync_loop    the same for K above 64 and the separate sync at K = 3
+//                  (other K take k_sync_lds, compiled for powers of two up to
+//                  32 or with K as an argument).
 //   k_reduce_chunks,  fixed-order sums of the tile partials per chunk, then
 //   k_reduce_windows  per tensor (in windows of tensors when there are more
 //   k_reduce_finish   chunk partials than one block's LDS holds) and over
@@ -201,12 +201,39 @@ __device__ __forceinline__ f4 tree_sum_regs(const f4 *v, int base) {
     }
 }
 
+// The pairwise tree over a run-time number (1 to 16) of LDS entries.
+__device__ __forceinline__ f4 tree_sum_lds_n(const f4 (*rows)[64], int lane, int n) {
+    switch (n) {
+    case 1: return tree_sum_lds<1>(rows, lane, 0);
+    case 2: return tree_sum_lds<2>(rows, lane, 0);
+    case 3: return tree_sum_lds<3>(rows, lane, 0);
+    case 4: return tree_sum_lds<4>(rows, lane, 0);
+    case 5: return tree_sum_lds<5>(rows, lane, 0);
+    case 6: return tree_sum_lds<6>(rows, lane, 0);
+    case 7: return tree_sum_lds<7>(rows, lane, 0);
+    case 8: return tree_sum_lds<8>(rows, lane, 0);
+    case 9: return tree_sum_lds<9>(rows, lane, 0);
+    case 10: return tree_sum_lds<10>(rows, lane, 0);
+    case 11: return tree_sum_lds<11>(rows, lane, 0);
+    case 12: return tree_sum_lds<12>(rows, lane, 0);
+    case 13: return tree_sum_lds<13>(rows, lane, 0);
+    case 14: return tree_sum_lds<14>(rows, lane, 0);
+    case 15: return tree_sum_lds<15>(rows, lane, 0);
+    default: return tree_sum_lds<16>(rows, lane, 0);
+    }
+}
+
 // The replica mean at one lane from the W wave sums in LDS: the pairwise tree
-// of a compiled K (WC = W waves), else the sums in wave order.
-template <int KT, int WC>
+// (WC = W waves for a compiled K, else W from K), so that with R rows per wave
+// the mean is the K-row tree when K is a power of two and exact for equal
+// replicas; with one row per wave (RD = 1, K = 3) the rows in row order, as
+// the loop kernel adds them.
+template <int KT, int WC, int RD>
 __device__ __forceinline__ f4 lds_mean(const f4 (*rows)[64], int lane, int W, int K) {
     if constexpr (KT > 0) {
         return tree_sum_lds<WC>(rows, lane, 0) / splat((float)KT);
+    } else if constexpr (RD > 1) {
+        return tree_sum_lds_n(rows, lane, W) / splat((float)K);
     } else {
         // the reads go out four at a time, and the adds run in wave order
         f4 s = rows[0][lane];
@@ -246,9 +273,9 @@ __device__ __forceinline__ bool device_due(const SyncParams &p) {
 // use masked scalar accesses.
 // Waves per block: one per worker row (at most 16) when the rows are stepped;
 // the averaging-only mode does best with two rows per wave (measured +2 to +15%).
-// KT = 0: K is a kernel argument (a K up to 32 without a compiled variant,
-// with RD = 2 rows per wave, or K = 3 with one); the W wave sums are then
-// added in wave order, and the mean of equal replicas need not be exact.
+// KT = 0: K is a kernel argument (a K up to 64 without a compiled variant,
+// with RD = 2 or 4 rows per wave, or K = 3 with one); see lds_mean for the
+// order of the mean.
 template <int KT, int MODE>
 constexpr int sync_waves() {
     if constexpr (KT == 0) return 16;  // the most waves a block of the K-argument kernel has
@@ -278,12 +305,12 @@ __device__ __forceinline__ Pair block_sum2_waves(double a, double b, int waves) 
     return total;
 }
 
-// RAGGED (K an argument, odd K, two rows per wave): the last wave holds one
-// row and publishes it alone; the mean adds the (K + 1) / 2 entries in order.
+// RAGGED (K an argument, K not a multiple of RD): the last wave holds fewer
+// rows; the missing ones count as zeros in its sum.
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD = 0, bool RAGGED = false>
 __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(SyncParams p) {
     static_assert((KT == 0) == (RD > 0), "RD (rows per wave) is given exactly when K is an argument");
-    static_assert(!RAGGED || RD == 2, "a ragged last wave comes with two rows per wave");
+    static_assert(!RAGGED || RD >= 2, "a ragged last wave comes with several rows per wave");
     constexpr int WMAX = sync_waves<KT, MODE>();
     constexpr int R = KT > 0 ? KT / WMAX : RD;
     const int W = KT > 0 ? WMAX : (p.s.K + (RD > 0 ? RD : 1) - 1) / (RD > 0 ? RD : 1);
@@ -345,21 +372,16 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
                 }
             }
         }
-        if (measure) {
-            if (RAGGED && !has[R - 1]) {  // the last wave of an odd K: one row
-                part[w][lane] = xr[0];
-                if (AVGM) mpart[w][lane] = m[0];
-            } else {
-                part[w][lane] = tree_sum_regs<R>(xr, 0);
-                if (AVGM) mpart[w][lane] = tree_sum_regs<R>(m, 0);
-            }
+        if (measure) {  // (rows a ragged last wave lacks hold zeros)
+            part[w][lane] = tree_sum_regs<R>(xr, 0);
+            if (AVGM) mpart[w][lane] = tree_sum_regs<R>(m, 0);
         }
     }
     if (!measure) return;  // uniform over the block
     __syncthreads();
     double acc = 0.0, gn = 0.0;
     if (active) {
-        const f4 mean = lds_mean<KT, WMAX>(part, lane, W, a.K);
+        const f4 mean = lds_mean<KT, WMAX, RD>(part, lane, W, a.K);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             if (!has[r]) continue;
@@ -374,7 +396,7 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (avg_m) {
-            const f4 mmean = lds_mean<KT, WMAX>(mpart, lane, W, a.K);
+            const f4 mmean = lds_mean<KT, WMAX, RD>(mpart, lane, W, a.K);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 if (!has[r]) continue;
@@ -813,17 +835,18 @@ size_t static_lds_of(Kern kern) {
 }
 
 // Does the K-argument sync-tile kernel take K in this mode (else the loop
-// kernel does)?  Two rows per wave (K up to 32; the last wave of an odd K
-// holds one): a CU holds at most two blocks of 9-16 waves, and two rows per
-// wave keep twice the bytes in flight.  K = 3 is the exception: one row per
-// wave in the modes with a step, and the loop kernel for the separate sync
-// (76% of peak, against 58% and 48% for three one-row or two two-row waves);
-// both add the rows in row order, so the replicas keep the same bits.
+// kernel does)?  Two rows per wave up to K = 32 and four up to 64 (the last
+// wave of a K that is not a multiple holds fewer): a CU holds at most two
+// blocks of 9-16 waves, and several rows per wave keep more bytes in flight.
+// K = 3 is the exception: one row per wave in the modes with a step, and the
+// loop kernel for the separate sync (76% of peak, against 58% and 48% for
+// three one-row or two two-row waves); both add the rows in row order, so the
+// replicas keep the same bits.
 constexpr bool any_k_kernel(int K, int mode) {
     if (K == 3) return mode != kAverage;
-    return K > 0 && K <= 32;
+    return K > 0 && K <= 64;
 }
-constexpr int any_k_rows(int K) { return K == 3 ? 1 : 2; }
+constexpr int any_k_rows(int K) { return K == 3 ? 1 : (K <= 32 ? 2 : 4); }
 constexpr int any_k_waves(int K) { return (K + any_k_rows(K) - 1) / any_k_rows(K); }
 
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD, bool RAGGED>
@@ -941,9 +964,15 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
     case 32: return sync_dispatch<32>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
     default:
         if (!any_k_kernel(p.s.K, mode)) return loop_dispatch(p, n_tiles, mode, avg_m, vec, st);
-        if (any_k_rows(p.s.K) == 1) return sync_dispatch<0, 1, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
-        if (p.s.K % 2 == 0) return sync_dispatch<0, 2, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
-        return sync_dispatch<0, 2, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);  // odd K, ragged
+        switch (any_k_rows(p.s.K)) {
+        case 1: return sync_dispatch<0, 1, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        case 2:
+            return p.s.K % 2 == 0 ? sync_dispatch<0, 2, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st)
+                                  : sync_dispatch<0, 2, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        default:
+            return p.s.K % 4 == 0 ? sync_dispatch<0, 4, false>(p, n_tiles, mode, avg_m, vec, nt, cap, st)
+                                  : sync_dispatch<0, 4, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
+        }
     }
 }
 

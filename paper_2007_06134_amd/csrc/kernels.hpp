@@ -102,7 +102,7 @@ enum SyncMode : int { kAverage = 0, kFused = 1, kDevice = 2, kDeviceTrace = 3 };
 // the mean; the latter only when tracing).  avg_m = true: a sync also averages
 // the momentum buffers.  cap > 0 reserves LDS (160 KB per CU on gfx950) so
 // that at most cap blocks of the sync-tile kernel are resident per CU; 0: none.
-// The loop kernel (K above 32, the separate sync at K = 3) ignores it.
+// The loop kernel (K above 64, the separate sync at K = 3) ignores it.
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec,
                             bool nontemporal, int cap, hipStream_t st);
 // Waves per block of the sync-tile kernel for K workers in a mode (0 when K
