@@ -40,15 +40,17 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(w, block, lds):
+def measured_traffic(w, block, lds, row_chunks):
     """HBM bytes per local-step launch from the committed counter summary, if it
     was taken on the current kernel sources, this problem (K = 8, P = 138M) and
-    this launch shape (threads per block, LDS reserved per block); else None."""
+    this launch shape (threads per block, LDS reserved per block, chunks per
+    row run); else None."""
     if (w.K, w.P) != (8, 138_000_000) or not os.path.exists(TRAFFIC_FILE):
         return None
     txt = open(TRAFFIC_FILE).read()
     m_d = re.search(r"kernel sources digest:\s*`?([0-9a-f]{16})", txt)
-    m_b = re.search(rf"HBM bytes per launch \(scaled\), block {block}, LDS {lds}:\s*([0-9.eE+]+)", txt)
+    m_b = re.search(rf"HBM bytes per launch \(scaled\), block {block}, LDS {lds}, row chunks {row_chunks}:"
+                    r"\s*([0-9.eE+]+)", txt)
     if not (m_d and m_b) or m_d.group(1) != kernel_source_digest():
         return None
     return float(m_b.group(1))
@@ -118,10 +120,10 @@ def main():
                     help="HIP events around every N-th launch of each kernel kind (default 8)")
     ap.add_argument("--traced", action="store_true",
                     help="run the tracing mode (per-step variance and gradient norm) instead")
-    ap.add_argument("--step-launch", default=None, metavar="BLOCK,LDS",
+    ap.add_argument("--step-launch", default=None, metavar="BLOCK,LDS[,ROWCHUNKS]",
                     help="fix the plain local step's launch shape (threads per block, LDS bytes reserved "
-                         "per block) instead of the one timed fastest at init, e.g. so that separate "
-                         "counter passes profile the same kernel")
+                         "per block, chunks of a row an XCD takes in a run; default 1) instead of the one "
+                         "timed fastest at init, e.g. so that separate counter passes profile the same kernel")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (x3), to scale byte counters")
     args = ap.parse_args()
@@ -147,8 +149,7 @@ def main():
     N = w.total_steps
     eng = A.Adpsgd.from_workload(w, device="cuda:0")
     if args.step_launch:
-        block, lds = (int(v) for v in args.step_launch.split(","))
-        eng.set_step_launch(block, lds)
+        eng.set_step_launch(*(int(v) for v in args.step_launch.split(",")))
     stream = eng.stream
 
     def one_run():
@@ -171,7 +172,7 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     tm = eng.get_timing()
-    step_block, step_lds = eng.step_launch
+    step_block, step_lds, step_row_chunks = eng.step_launch
     row_stride = eng.row_stride
     sep = None
     if not args.no_timing:
@@ -216,9 +217,10 @@ def main():
         step_ms = tm.step_ms / tm.step_launches
         achieved = step_bytes / (step_ms * 1e-3) / 1e9
         out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w, step_block, step_lds),
+                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w, step_block, step_lds, step_row_chunks),
                            "kernel": f"k_local_step<{step_block}>",
-                           "lds_reserved_per_block": step_lds, "row_stride": row_stride,
+                           "lds_reserved_per_block": step_lds, "row_chunks": step_row_chunks,
+                           "row_stride": row_stride,
                            "bytes_per_launch": step_bytes,
                            "avg_launch_ms": step_ms, "timed_launches": tm.step_launches,
                            "timed_every": args.timing_every}

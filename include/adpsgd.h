@@ -265,16 +265,21 @@ ADPSGD_API int adpsgd_get_state(const adpsgd_ctx *c, adpsgd_state *out);
 ADPSGD_API int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in);
 
 /* Launch shape of the plain local step: block = 64, 128 or 256 threads (float4
- * groups of one worker's row per workgroup), and lds_bytes of LDS reserved per
- * block, which the kernel does not use: it only holds each CU to
- * floor(160 KB / lds_bytes) resident blocks (0: no reservation).  The fastest
- * shape differs with the problem and the machine, so when K * P >= 2^24
- * adpsgd_init times (64, 0), (64, 8192), (128, 0) and (256, 0) on the context's
- * buffers and keeps the fastest (else (256, 0)).  set: block 64, 128 or 256 with
- * lds_bytes in [0, 65536], or block 0 for the timed choice (lds_bytes ignored);
- * every shape computes the same bits.  EINVAL otherwise. */
-ADPSGD_API int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes);
-ADPSGD_API int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes);
+ * groups of one worker's row per workgroup, a chunk); lds_bytes of LDS reserved
+ * per block, which the kernel does not use: it only holds each CU to
+ * floor(160 KB / lds_bytes) resident blocks (0: no reservation); and
+ * row_chunks = S, the block order: the K blocks of a chunk run on one XCD, and
+ * an XCD takes S chunks of one worker's row before the same S chunks of the
+ * next worker's (1: the K workers of each chunk in turn).  The fastest shape
+ * differs with the problem and the machine, so when K * P >= 2^24 adpsgd_init
+ * times (64, 0, 1), (64, 8192, 1), (128, 0, 1), (256, 0, 1), (64, 8192, 16),
+ * (64, 8192, 32) and (64, 8192, 64) on the context's buffers and keeps the
+ * fastest (else (256, 0, 1)).  set: block 64, 128 or 256 with lds_bytes in
+ * [0, 65536] and row_chunks in [1, 4096], or block 0 for the timed choice (the
+ * others ignored); every shape computes the same bits.  EINVAL otherwise. */
+ADPSGD_API int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes, int32_t row_chunks);
+ADPSGD_API int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes,
+                                      int32_t *row_chunks);
 
 /* How adpsgd_run launches its steps (ADPSGD_LAUNCH_*); every policy computes the
  * same results.  EINVAL for an unknown policy. */

@@ -113,11 +113,12 @@ class Adpsgd:
 
     @property
     def step_launch(self) -> tuple:
-        """(threads per block, LDS bytes reserved per block) of the plain local step."""
+        """(threads per block, LDS bytes reserved per block, chunks of a row an
+        XCD takes in a run) of the plain local step."""
         return adpsgd_get_step_launch(self.ctx)
 
-    def set_step_launch(self, block: int, lds_bytes: int = 0) -> None:
-        adpsgd_set_step_launch(self.ctx, block, lds_bytes)
+    def set_step_launch(self, block: int, lds_bytes: int = 0, row_chunks: int = 1) -> None:
+        adpsgd_set_step_launch(self.ctx, block, lds_bytes, row_chunks)
 
     def set_launch_policy(self, policy: int) -> None:
         adpsgd_set_launch_policy(self.ctx, policy)

@@ -110,8 +110,8 @@ _SIGS = {
     "adpsgd_get_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
     "adpsgd_set_state": (C.c_int, [_CTX, C.POINTER(adpsgd_state)]),
     "adpsgd_set_launch_policy": (C.c_int, [_CTX, C.c_int32]),
-    "adpsgd_set_step_launch": (C.c_int, [_CTX, C.c_int32, C.c_int32]),
-    "adpsgd_get_step_launch": (C.c_int, [_CTX, C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+    "adpsgd_set_step_launch": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32]),
+    "adpsgd_get_step_launch": (C.c_int, [_CTX, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
     "adpsgd_set_timing": (C.c_int, [_CTX, C.c_int32]),
     "adpsgd_get_timing": (C.c_int, [_CTX, C.POINTER(adpsgd_timing)]),
     "adpsgd_destroy": (C.c_int, [_CTX]),
@@ -252,14 +252,15 @@ def adpsgd_set_state(ctx: int, st: adpsgd_state) -> None:
     _check(lib.adpsgd_set_state(ctx, C.byref(st)))
 
 
-def adpsgd_set_step_launch(ctx: int, block: int, lds_bytes: int = 0) -> None:
-    _check(lib.adpsgd_set_step_launch(ctx, block, lds_bytes))
+def adpsgd_set_step_launch(ctx: int, block: int, lds_bytes: int = 0, row_chunks: int = 1) -> None:
+    _check(lib.adpsgd_set_step_launch(ctx, block, lds_bytes, row_chunks))
 
 
 def adpsgd_get_step_launch(ctx: int) -> tuple:
-    b, s = C.c_int32(), C.c_int32()
-    _check(lib.adpsgd_get_step_launch(ctx, C.byref(b), C.byref(s)))
-    return b.value, s.value
+    """(threads per block, LDS bytes reserved per block, chunks per row run)."""
+    b, s, r = C.c_int32(), C.c_int32(), C.c_int32()
+    _check(lib.adpsgd_get_step_launch(ctx, C.byref(b), C.byref(s), C.byref(r)))
+    return b.value, s.value, r.value
 
 
 def adpsgd_set_launch_policy(ctx: int, policy: int) -> None:

@@ -135,19 +135,23 @@ __device__ __forceinline__ double grad_norm2(const StepParams &a, f4 mean, f4 h,
 
 // ---------------------------------------------------------------- local step
 
-// Thread = (group g, worker k); a block covers BS consecutive groups of one
-// worker's row.  Blocks are ordered so that the K blocks of a BS-group chunk
-// are dispatched to the same XCD one after another (workgroups go round-robin
-// over the 8 XCDs): h and x* of the chunk come from HBM once and from that
-// XCD's L2 for the other K-1 workers.  The best BS depends on the shape and
-// the machine (64, 128 and 256 each win somewhere); the runtime times them.
+// Thread = (group g, worker k); a block covers BS consecutive groups (a
+// chunk) of one worker's row.  Workgroups go round-robin over the 8 XCDs, and
+// the blocks are ordered so that the K blocks of a chunk run on the same XCD:
+// h and x* of the chunk come from HBM once and from that XCD's L2 for the
+// other K-1 workers.  Within an XCD, S = row_chunks chunks of one worker's
+// row come one after another, then the same S chunks of the next worker's
+// row, so each row is streamed in runs of S chunks (S = 1: the K workers of
+// one chunk in turn).  The best BS, S and LDS reservation depend on the shape
+// and the machine; the runtime times a few.
 // TAIL: P is not a multiple of 4, so the last group of every row is partial.
 template <int BS, bool VEC, bool NT, bool TAIL>
 __global__ void __launch_bounds__(BS) k_local_step(StepParams a) {
     const int64_t b = a.block0 + blockIdx.x;
     const int64_t s = b >> 3;                        // position within the XCD
-    const int k = (int)(s % a.K);
-    const int64_t chunk = (s / a.K) * 8 + (b & 7);
+    const int64_t run = s / a.row_chunks;            // (super-chunk, worker)
+    const int k = (int)(run % a.K);
+    const int64_t chunk = ((run / a.K) * a.row_chunks + (s - run * a.row_chunks)) * 8 + (b & 7);
     const int64_t g = chunk * BS + threadIdx.x;
     if (g >= a.n_groups) return;
     const int64_t e0 = 4 * g;
@@ -908,16 +912,19 @@ hipError_t loop_dispatch(const SyncParams &p, int64_t n_tiles, int mode, bool av
 
 }  // namespace
 
-int64_t local_step_blocks(int64_t n_groups, int32_t K, int block) {
-    const int64_t chunks = (n_groups + block - 1) / block;
-    return ((chunks + 7) / 8) * 8 * (int64_t)K;
+int64_t local_step_blocks(int64_t n_groups, int32_t K, const StepShape &shape) {
+    const int64_t chunks = (n_groups + shape.block - 1) / shape.block;
+    const int64_t per = 8 * (int64_t)shape.row_chunks;  // chunks of one super-chunk
+    return ((chunks + per - 1) / per) * per * (int64_t)K;
 }
 
 template <int BS>
-hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, int lds, hipStream_t st) {
-    // lds: dynamic LDS per block that the kernel never touches (an occupancy cap)
-    return in_pieces(local_step_blocks(p.n_groups, p.K, BS), BS, [&](int64_t b0, unsigned nb) {
+hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, const StepShape &shape, hipStream_t st) {
+    // shape.lds: dynamic LDS per block that the kernel never touches (an occupancy cap)
+    const int lds = shape.lds;
+    return in_pieces(local_step_blocks(p.n_groups, p.K, shape), BS, [&](int64_t b0, unsigned nb) {
         StepParams q = p;
+        q.row_chunks = shape.row_chunks;
         q.block0 = b0;
         const bool tail = (p.P & 3) != 0;
         if (vec && nt && tail) k_local_step<BS, true, true, true><<<dim3(nb), dim3(BS), lds, st>>>(q);
@@ -928,13 +935,14 @@ hipError_t local_step_bs(const StepParams &p, bool vec, bool nt, int lds, hipStr
     });
 }
 
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, int block, int lds, hipStream_t st) {
-    if (lds < 0 || lds > kMaxStepLds) return hipErrorInvalidValue;
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nt, const StepShape &shape, hipStream_t st) {
+    if (shape.lds < 0 || shape.lds > kMaxStepLds) return hipErrorInvalidValue;
+    if (shape.row_chunks < 1 || shape.row_chunks > kMaxRowChunks) return hipErrorInvalidValue;
     if (p.n_groups <= 0) return hipSuccess;
-    switch (block) {
-    case 64: return local_step_bs<64>(p, vec, nt, lds, st);
-    case 128: return local_step_bs<128>(p, vec, nt, lds, st);
-    case 256: return local_step_bs<256>(p, vec, nt, lds, st);
+    switch (shape.block) {
+    case 64: return local_step_bs<64>(p, vec, nt, shape, st);
+    case 128: return local_step_bs<128>(p, vec, nt, shape, st);
+    case 256: return local_step_bs<256>(p, vec, nt, shape, st);
     default: return hipErrorInvalidValue;
     }
 }

@@ -54,6 +54,11 @@ struct StepParams {
     uint32_t t;        // step index (Philox counter word 2)
     float sigma, mu, wd, gamma;
     RoundKeys rk;
+    // Chunks of one worker's row that an XCD takes one after another before
+    // the next worker's (the local step's block order; set by
+    // launch_local_step, ignored by the sync kernels).
+    int32_t row_chunks;
+    int32_t pad_;
     // First block of this launch: a dispatch counts its grid in 32-bit
     // work-items, so larger grids go out as several launches (the launchers
     // below set it; callers leave it 0).
@@ -72,23 +77,33 @@ struct SyncParams {
 };
 
 // Launch shapes of the local step: threads per block (= float4 groups per
-// block) and an LDS reservation per block.  The kernel uses no LDS; the
-// reservation only holds a CU to floor(160 KB / lds) resident blocks, and
-// fewer waves in flight can stream HBM slightly faster.  The grid size for
-// n_groups groups, K workers and a block size is local_step_blocks.
+// block), an LDS reservation per block, and the block order.  The kernel uses
+// no LDS; the reservation only holds a CU to floor(160 KB / lds) resident
+// blocks, and fewer waves in flight can stream HBM slightly faster.  The
+// blocks of a chunk (block groups of every worker's row) go to one XCD;
+// row_chunks = S: an XCD takes S chunks of one worker's row, then the same S
+// chunks of the next worker's, so that each row is streamed in longer runs.
+// The grid size for n_groups groups, K workers and a shape is
+// local_step_blocks.
 struct StepShape {
     int block;
     int lds;
+    int row_chunks;
 };
 constexpr int kStepBlocks[] = {64, 128, 256};
 constexpr int kMaxStepLds = 64 * 1024;
-// The shapes adpsgd_init times: the three block sizes, and 64-thread blocks
-// held to 20 per CU (8 KB each).
-constexpr StepShape kStepShapes[] = {{64, 0}, {64, 8192}, {128, 0}, {256, 0}};
-int64_t local_step_blocks(int64_t n_groups, int32_t K, int block);
-// vec: rows are 16-byte aligned (row stride % 4 == 0) so full groups use dwordx4;
-// block: one of kStepBlocks, lds in [0, kMaxStepLds] (hipErrorInvalidValue otherwise).
-hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, int block, int lds, hipStream_t st);
+constexpr int kMaxRowChunks = 4096;
+// The shapes adpsgd_init times: the three block sizes with one chunk per row
+// run, 64-thread blocks held to 20 per CU (8 KB each), and those with runs of
+// 16, 32 and 64 chunks.
+constexpr StepShape kStepShapes[] = {{64, 0, 1},     {64, 8192, 1},  {128, 0, 1},   {256, 0, 1},
+                                     {64, 8192, 16}, {64, 8192, 32}, {64, 8192, 64}};
+int64_t local_step_blocks(int64_t n_groups, int32_t K, const StepShape &shape);
+// vec: rows are 16-byte aligned (row stride % 4 == 0) so full groups use
+// dwordx4; shape: block one of kStepBlocks, lds in [0, kMaxStepLds],
+// row_chunks in [1, kMaxRowChunks] (hipErrorInvalidValue otherwise).
+hipError_t launch_local_step(const StepParams &p, bool vec, bool nontemporal, const StepShape &shape,
+                             hipStream_t st);
 // What a sync-tile kernel does:
 //   kAverage      average only (a separate sync);
 //   kFused        one local step, then average (a period's last step);

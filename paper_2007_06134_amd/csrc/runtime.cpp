@@ -234,8 +234,8 @@ struct adpsgd_ctx {
     bool vec = true;                // row stride % 4 == 0: rows 16-byte aligned, dwordx4 groups
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
-    StepShape step_shape{256, 0};   // launch shape of the plain local step in use
-    StepShape tuned_shape{256, 0};  // the fastest one measured at init
+    StepShape step_shape{256, 0, 1};   // launch shape of the plain local step in use
+    StepShape tuned_shape{256, 0, 1};  // the fastest one measured at init
     int32_t average_cap = 0;        // resident blocks per CU of the separate sync (0: no cap), timed at init
     RoundKeys rk{};
     bool timing = false;
@@ -355,6 +355,8 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
     p.wd = (float)c->hp.weight_decay;
     p.gamma = (float)adpsgd_lr(&c->hp, t);
     p.rk = c->rk;
+    p.row_chunks = 1;  // set by launch_local_step from the launch shape
+    p.pad_ = 0;
     p.block0 = 0;
     return p;
 }
@@ -362,7 +364,7 @@ StepParams step_params(const adpsgd_ctx *c, int64_t t) {
 int enqueue_steps(adpsgd_ctx *c, int64_t t0, int64_t n) {
     for (int64_t j = 0; j < n; ++j) {
         const StepParams p = step_params(c, t0 + j);
-        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->step_shape.block, c->step_shape.lds, c->stream); });
+        int rc = timed_launch(c, tStep, [&] { return launch_local_step(p, c->vec, c->nontemporal, c->step_shape, c->stream); });
         if (rc) return rc;
     }
     return ok();
@@ -490,7 +492,7 @@ hipError_t tune_step_shape(adpsgd_ctx *c) {
     float best[n];
     for (int j = 0; j < n; ++j) best[j] = 3.4e38f;
     auto launch = [&](int j) {
-        return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j].block, kStepShapes[j].lds, c->stream);
+        return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j], c->stream);
     };
     for (int j = 0; j < n && e == hipSuccess; ++j) e = launch(j);
     for (int round = 0; round < 5 && e == hipSuccess; ++round) {
@@ -955,7 +957,7 @@ extern "C" int adpsgd_set_state(adpsgd_ctx *c, const adpsgd_state *in) {
     return ok();
 }
 
-extern "C" int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes) {
+extern "C" int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_bytes, int32_t row_chunks) {
     if (int rc = check_ctx(c)) return rc;
     if (block == 0) {
         c->step_shape = c->tuned_shape;
@@ -965,15 +967,18 @@ extern "C" int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_
     for (int b : kStepBlocks) known = known || b == block;
     if (!known) return fail(ADPSGD_EINVAL, "block must be 0, 64, 128 or 256");
     if (lds_bytes < 0 || lds_bytes > kMaxStepLds) return fail(ADPSGD_EINVAL, "lds_bytes must be in [0, 65536]");
-    c->step_shape = StepShape{block, lds_bytes};
+    if (row_chunks < 1 || row_chunks > kMaxRowChunks) return fail(ADPSGD_EINVAL, "row_chunks must be in [1, 4096]");
+    c->step_shape = StepShape{block, lds_bytes, row_chunks};
     return ok();
 }
 
-extern "C" int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes) {
+extern "C" int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes,
+                                      int32_t *row_chunks) {
     if (int rc = check_ctx(c)) return rc;
-    if (!block || !lds_bytes) return fail(ADPSGD_EINVAL, "block or lds_bytes is NULL");
+    if (!block || !lds_bytes || !row_chunks) return fail(ADPSGD_EINVAL, "block, lds_bytes or row_chunks is NULL");
     *block = c->step_shape.block;
     *lds_bytes = c->step_shape.lds;
+    *row_chunks = c->step_shape.row_chunks;
     return ok();
 }
 

@@ -36,10 +36,11 @@ static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t 
     OKC(adpsgd_init(K, P, off.data(), T, &hp, &b, &c));
     OKC(adpsgd_set_launch_policy(c, policy));
     OKC(adpsgd_set_timing(c, 3));
-    int32_t blk = 0, lds = 0;
-    OKC(adpsgd_get_step_launch(c, &blk, &lds));
-    OKC(adpsgd_set_step_launch(c, 64, 8192));
-    if (adpsgd_set_step_launch(c, 96, 0) != ADPSGD_EINVAL || adpsgd_get_step_launch(c, &blk, nullptr) != ADPSGD_EINVAL) {
+    int32_t blk = 0, lds = 0, rch = 0;
+    OKC(adpsgd_get_step_launch(c, &blk, &lds, &rch));
+    OKC(adpsgd_set_step_launch(c, 64, 8192, 32));
+    if (adpsgd_set_step_launch(c, 96, 0, 1) != ADPSGD_EINVAL || adpsgd_set_step_launch(c, 64, 0, 0) != ADPSGD_EINVAL ||
+        adpsgd_get_step_launch(c, &blk, nullptr, &rch) != ADPSGD_EINVAL) {
         printf("expected EINVAL\n"); return 1;
     }
     std::vector<adpsgd_sync_rec> log(N);
@@ -64,7 +65,7 @@ static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t 
     // error paths leave the context usable
     if (adpsgd_run(c, -1, nullptr, 0, nullptr, nullptr) != ADPSGD_EINVAL) { printf("expected EINVAL\n"); return 1; }
     if (adpsgd_set_launch_policy(c, 9) != ADPSGD_EINVAL) { printf("expected EINVAL\n"); return 1; }
-    OKC(adpsgd_set_step_launch(c, 0, 0));
+    OKC(adpsgd_set_step_launch(c, 0, 0, 0));
     OKC(adpsgd_reset(c));
     OKC(adpsgd_run(c, 5, nullptr, 0, nullptr, &n));
     OKC(adpsgd_destroy(c));

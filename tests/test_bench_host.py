@@ -19,7 +19,8 @@ def bench():
 
 def _summary(digest, shapes):
     lines = [f"kernel sources digest: `{digest}`", ""]
-    lines += [f"HBM bytes per launch (scaled), block {b}, LDS {l}: {v:.6e}" for (b, l), v in shapes.items()]
+    lines += [f"HBM bytes per launch (scaled), block {b}, LDS {l}, row chunks {r}: {v:.6e}"
+              for (b, l, r), v in shapes.items()]
     return "\n".join(lines) + "\n"
 
 
@@ -28,15 +29,16 @@ def test_traffic_is_read_for_the_launch_shape_and_current_sources(bench, tmp_pat
     assert (w.K, w.P) == (8, 138_000_000)
     f = tmp_path / "traffic.md"
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
-    shapes = {(64, 0): 1.8768e10, (64, 8192): 1.8769e10, (128, 0): 1.877e10}
+    shapes = {(64, 0, 1): 1.8768e10, (64, 8192, 1): 1.8769e10, (128, 0, 1): 1.877e10, (64, 8192, 32): 1.8771e10}
     f.write_text(_summary(bench.kernel_source_digest(), shapes))
-    for (b, l), v in shapes.items():
-        assert bench.measured_traffic(w, b, l) == pytest.approx(v, rel=1e-6)
-    assert bench.measured_traffic(w, 256, 0) is None          # shape not profiled
-    assert bench.measured_traffic(w, 64, 819) is None         # no prefix match of the LDS figure
+    for (b, l, r), v in shapes.items():
+        assert bench.measured_traffic(w, b, l, r) == pytest.approx(v, rel=1e-6)
+    assert bench.measured_traffic(w, 256, 0, 1) is None       # shape not profiled
+    assert bench.measured_traffic(w, 64, 8192, 3) is None     # no prefix match of a figure
+    assert bench.measured_traffic(w, 64, 819, 1) is None
     f.write_text(_summary("0" * 16, shapes))                  # counters from other sources
-    assert bench.measured_traffic(w, 64, 0) is None
-    assert bench.measured_traffic(W.parity_workloads()["resnet18_like"], 64, 0) is None
+    assert bench.measured_traffic(w, 64, 0, 1) is None
+    assert bench.measured_traffic(W.parity_workloads()["resnet18_like"], 64, 0, 1) is None
 
 
 def test_more_than_one_gpu_is_refused(bench, monkeypatch, capsys):

@@ -361,7 +361,9 @@ def test_manual_algorithm2_loop_equals_run(A, key, fused):
     assert st.C2 == pytest.approx(g["state"].C2, rel=1e-12)
 
 
-STEP_SHAPES = [(64, 0), (64, 8192), (128, 0), (256, 0), (256, 65536)]
+STEP_SHAPES = [(64, 0, 1), (64, 8192, 1), (128, 0, 1), (256, 0, 1), (64, 8192, 16), (64, 8192, 32),
+               (64, 8192, 64), (256, 65536, 1), (128, 0, 4096), (64, 0, 3)]
+TIMED_SHAPES = STEP_SHAPES[:7]
 
 
 def test_step_launch_shapes_agree_bitwise(A):
@@ -381,14 +383,14 @@ def test_step_launch_shapes_agree_bitwise(A):
     assert all(runs[s] == runs[STEP_SHAPES[0]] for s in STEP_SHAPES)
     with A.Adpsgd.from_workload(w) as eng:
         tuned = eng.step_launch
-        assert tuned in STEP_SHAPES[:4]
-        for bad in [(96, 0), (64, -1), (64, 65537)]:
+        assert tuned in TIMED_SHAPES
+        for bad in [(96, 0, 1), (64, -1, 1), (64, 65537, 1), (64, 0, 0), (64, 0, 4097)]:
             with pytest.raises(A.AdpsgdError) as e:
                 eng.set_step_launch(*bad)
             assert e.value.code == A.EINVAL
             assert eng.step_launch == tuned
-        eng.set_step_launch(256, 4096)
-        eng.set_step_launch(0, 123)                # back to the timed choice
+        eng.set_step_launch(256, 4096, 2)
+        eng.set_step_launch(0, 123, 0)             # back to the timed choice
         assert eng.step_launch == tuned
 
 
