@@ -480,76 +480,70 @@ hipError_t zero_rows(const adpsgd_ctx *c) {
     return e;
 }
 
-// Time the local step in every launch shape on the context's own buffers (the
-// launches step x and m, which the caller zeroes afterwards): one warm-up
-// launch each, then five interleaved rounds; the fastest minimum wins.
-hipError_t tune_step_shape(adpsgd_ctx *c) {
-    const StepParams p = step_params(c, 0);
-    constexpr int n = (int)(sizeof(kStepShapes) / sizeof(kStepShapes[0]));
-    hipEvent_t a = nullptr, b = nullptr;
-    hipError_t e = hipEventCreate(&a);
-    if (e == hipSuccess) e = hipEventCreate(&b);
-    float best[n];
+// The fastest of n launch variants on the context's stream: one warm-up launch
+// each, then five rounds; a round queues every variant back to back with an
+// event between consecutive launches, so each interval is the GPU's time for
+// one launch (no host round trip inside it).  The fastest minimum wins.
+template <class Launch>
+hipError_t fastest_variant(adpsgd_ctx *c, int n, Launch launch, int *win) {
+    constexpr int kMaxVariants = 8;
+    if (n < 1 || n > kMaxVariants) return hipErrorInvalidValue;
+    hipEvent_t ev[kMaxVariants + 1] = {};
+    hipError_t e = hipSuccess;
+    for (int j = 0; j <= n && e == hipSuccess; ++j) e = hipEventCreate(&ev[j]);
+    float best[kMaxVariants];
     for (int j = 0; j < n; ++j) best[j] = 3.4e38f;
-    auto launch = [&](int j) {
-        return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j], c->stream);
-    };
     for (int j = 0; j < n && e == hipSuccess; ++j) e = launch(j);
     for (int round = 0; round < 5 && e == hipSuccess; ++round) {
+        e = hipEventRecord(ev[0], c->stream);
+        for (int j = 0; j < n && e == hipSuccess; ++j)
+            if ((e = launch(j)) == hipSuccess) e = hipEventRecord(ev[j + 1], c->stream);
+        if (e == hipSuccess) e = hipEventSynchronize(ev[n]);
         for (int j = 0; j < n && e == hipSuccess; ++j) {
             float ms = 0.f;
-            if ((e = hipEventRecord(a, c->stream)) != hipSuccess) break;
-            if ((e = launch(j)) != hipSuccess) break;
-            if ((e = hipEventRecord(b, c->stream)) != hipSuccess) break;
-            if ((e = hipEventSynchronize(b)) != hipSuccess) break;
-            if ((e = hipEventElapsedTime(&ms, a, b)) != hipSuccess) break;
-            best[j] = std::min(best[j], ms);
+            if ((e = hipEventElapsedTime(&ms, ev[j], ev[j + 1])) == hipSuccess) best[j] = std::min(best[j], ms);
         }
     }
     if (e == hipSuccess) {
-        int win = n - 1;
-        for (int j = 0; j < n; ++j)
-            if (best[j] < best[win]) win = j;
-        c->tuned_shape = c->step_shape = kStepShapes[win];
+        *win = 0;
+        for (int j = 1; j < n; ++j)
+            if (best[j] < best[*win]) *win = j;
     }
-    if (a) (void)hipEventDestroy(a);
-    if (b) (void)hipEventDestroy(b);
+    for (int j = 0; j <= n; ++j)
+        if (ev[j]) (void)hipEventDestroy(ev[j]);
+    return e;
+}
+
+// Time the local step in every launch shape on the context's own buffers (the
+// launches step x and m, which the caller zeroes afterwards).
+hipError_t tune_step_shape(adpsgd_ctx *c) {
+    const StepParams p = step_params(c, 0);
+    constexpr int n = (int)(sizeof(kStepShapes) / sizeof(kStepShapes[0]));
+    int win = 0;
+    const hipError_t e = fastest_variant(
+        c, n, [&](int j) { return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j], c->stream); }, &win);
+    if (e == hipSuccess) c->tuned_shape = c->step_shape = kStepShapes[win];
     return e;
 }
 
 // Time the separate sync (mean, broadcast and variance of every tile, no step)
 // without and with an LDS cap that holds a CU to kAverageCapWaves resident
-// waves, on the context's own buffers (zeroed again afterwards); one warm-up
-// launch each, then five interleaved rounds; the fastest minimum wins.
+// waves, on the context's own buffers (zeroed again afterwards).
 hipError_t tune_average_cap(adpsgd_ctx *c) {
     const int waves = sync_tile_waves(c->K, kAverage);
     if (waves <= 0 || c->tiles.empty()) return hipSuccess;
     const int caps[2] = {0, std::max(1, kAverageCapWaves / waves)};
     const SyncParams sp = sync_params(c, 0);
     const int64_t n_tiles = (int64_t)c->tiles.size();
-    auto launch = [&](int j) {
-        return launch_tile_sync(sp, n_tiles, kAverage, c->hp.avg_momentum != 0, c->vec, c->nontemporal, caps[j],
-                                c->stream);
-    };
-    hipEvent_t a = nullptr, b = nullptr;
-    hipError_t e = hipEventCreate(&a);
-    if (e == hipSuccess) e = hipEventCreate(&b);
-    float best[2] = {3.4e38f, 3.4e38f};
-    for (int j = 0; j < 2 && e == hipSuccess; ++j) e = launch(j);
-    for (int round = 0; round < 5 && e == hipSuccess; ++round) {
-        for (int j = 0; j < 2 && e == hipSuccess; ++j) {
-            float ms = 0.f;
-            if ((e = hipEventRecord(a, c->stream)) != hipSuccess) break;
-            if ((e = launch(j)) != hipSuccess) break;
-            if ((e = hipEventRecord(b, c->stream)) != hipSuccess) break;
-            if ((e = hipEventSynchronize(b)) != hipSuccess) break;
-            if ((e = hipEventElapsedTime(&ms, a, b)) != hipSuccess) break;
-            best[j] = std::min(best[j], ms);
-        }
-    }
-    if (e == hipSuccess) c->average_cap = best[1] < best[0] ? caps[1] : 0;
-    if (a) (void)hipEventDestroy(a);
-    if (b) (void)hipEventDestroy(b);
+    int win = 0;
+    const hipError_t e = fastest_variant(
+        c, 2,
+        [&](int j) {
+            return launch_tile_sync(sp, n_tiles, kAverage, c->hp.avg_momentum != 0, c->vec, c->nontemporal, caps[j],
+                                    c->stream);
+        },
+        &win);
+    if (e == hipSuccess) c->average_cap = caps[win];
     return e;
 }
 
