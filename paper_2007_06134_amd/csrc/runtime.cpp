@@ -484,9 +484,10 @@ hipError_t zero_rows(const adpsgd_ctx *c) {
 // each, then five rounds; a round queues every variant back to back with an
 // event between consecutive launches, so each interval is the GPU's time for
 // one launch (no host round trip inside it).  The fastest minimum wins.
+constexpr int kMaxVariants = 8;
+
 template <class Launch>
 hipError_t fastest_variant(adpsgd_ctx *c, int n, Launch launch, int *win) {
-    constexpr int kMaxVariants = 8;
     if (n < 1 || n > kMaxVariants) return hipErrorInvalidValue;
     hipEvent_t ev[kMaxVariants + 1] = {};
     hipError_t e = hipSuccess;
@@ -519,6 +520,7 @@ hipError_t fastest_variant(adpsgd_ctx *c, int n, Launch launch, int *win) {
 hipError_t tune_step_shape(adpsgd_ctx *c) {
     const StepParams p = step_params(c, 0);
     constexpr int n = (int)(sizeof(kStepShapes) / sizeof(kStepShapes[0]));
+    static_assert(n <= kMaxVariants, "more step shapes than the timing helper takes");
     int win = 0;
     const hipError_t e = fastest_variant(
         c, n, [&](int j) { return launch_local_step(p, c->vec, c->nontemporal, kStepShapes[j], c->stream); }, &win);
