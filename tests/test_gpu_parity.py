@@ -403,12 +403,18 @@ def test_step_launch_shapes_agree_bitwise(A, case):
         assert eng.step_launch == tuned
 
 
+N_RANDOM_SMALL_K, N_RANDOM_LARGE_K = 128, 32
+
+
 def _random_workload(i):
-    """A seeded random small configuration: K (odd ones take the any-K sync
-    kernel), 1-11 ragged tensors (empty ones included), period mode, LR
-    schedule, warm-up prefix, period switch and momentum averaging."""
+    """A seeded random small configuration: K (the first 128 cases up to 32,
+    the next 32 from 25 to 65: two and four rows per wave with ragged last
+    waves, and the loop kernel), 1-11 ragged tensors (empty ones included),
+    period mode, LR schedule, warm-up prefix, period switch and momentum
+    averaging."""
     rng = np.random.default_rng(7000 + i)
-    K = int(rng.choice([1, 2, 3, 4, 5, 7, 8, 12, 16, 24, 32]))
+    ks = [1, 2, 3, 4, 5, 7, 8, 12, 16, 24, 32] if i < N_RANDOM_SMALL_K else [25, 31, 33, 48, 64, 65]
+    K = int(rng.choice(ks))
     T = int(rng.integers(1, 12))
     sizes = [int(s) for s in rng.integers(0, 6000, size=T)]
     if sum(sizes) == 0:
@@ -428,7 +434,7 @@ def _random_workload(i):
     return W.Workload(**kw)
 
 
-@pytest.mark.parametrize("i", range(128))
+@pytest.mark.parametrize("i", range(N_RANDOM_SMALL_K + N_RANDOM_LARGE_K))
 def test_random_workloads_match_oracle(A, i):
     """128 seeded random configurations against the oracle (x, m, the sync
     list, S and the per-tensor variances).  The closest decision of these seeds
