@@ -57,7 +57,7 @@ extern "C" {
 #define ADPSGD_EINVAL (-1)     /* invalid argument; nothing was enqueued           */
 #define ADPSGD_ESTATE (-2)     /* call not valid in the context's current state    */
 #define ADPSGD_EDEVICE (-3)    /* a HIP runtime call failed (see adpsgd_last_error) */
-#define ADPSGD_ENONFINITE (-4) /* the variance S was NaN or infinite; p unchanged  */
+#define ADPSGD_ENONFINITE (-4) /* the variance S was NaN or infinite; p, C2 kept  */
 
 /* ---- learning-rate schedules: gamma_t for 0-based step t ------------------- */
 #define ADPSGD_LR_CONST 0  /* gamma_t = lr0                                             */
@@ -229,8 +229,9 @@ ADPSGD_API int adpsgd_step_average(adpsgd_ctx *c, double *var_out);
  * S = sum(var[0..T)), as adpsgd_sched_on_sync.  Sampling phase (t-1 < k_s):
  * C2 <- running mean of S / gamma; otherwise p + 1 if S < thr_lo gamma C2,
  * p - 1 if S > thr_hi gamma C2.  Constant mode and the warm-up prefix: no
- * change.  *next_period (may be NULL) receives p.  ENONFINITE, with the state
- * unchanged, if S is NaN or infinite. */
+ * change.  *next_period (may be NULL) receives p.  ENONFINITE if S is NaN or
+ * infinite: the counter still restarts (the sync took place), while p, C2 and
+ * nC2 are unchanged. */
 ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_period);
 
 /* Run n_steps steps of Algorithm 2 from the current state: local steps, a sync
@@ -333,8 +334,8 @@ ADPSGD_API int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int
 /* Apply Algorithm 2, lines 9 and 13-19, for a sync after step t with variance
  * S: cnt = 0; in adaptive mode after the warm-up prefix, C2 sampling (t < k_s)
  * or p +- 1.  *margin (may be NULL) receives the decision margin (NaN if no
- * decision).  ENONFINITE (state unchanged) if S is not finite; EINVAL on a
- * NULL pointer. */
+ * decision).  ENONFINITE if S is not finite: cnt = 0 as after every sync,
+ * with p, C2 and nC2 unchanged; EINVAL on a NULL pointer. */
 ADPSGD_API int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,
                          double *margin);
 

@@ -115,8 +115,8 @@ extern "C" int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, 
     double m = std::numeric_limits<double>::quiet_NaN();
     const bool finite = apply_sync(rule_of(hp), t, adpsgd_lr(hp, t), S, &s, &m);
     if (margin) *margin = m;
-    if (!finite) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
     st->cnt = s.cnt;
+    if (!finite) return fail(ADPSGD_ENONFINITE, "variance S is not finite");
     st->nC2 = s.nC2;
     st->C2 = s.C2;
     st->p = s.p;

@@ -733,12 +733,8 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r
         int32_t status = ADPSGD_OK, p_next = p_t;
         if (r.sched && due) {
             st.p = p_t;
-            if (!apply_sync(r.rule, r.t, r.gamma, tot.a, &st, nullptr)) {
-                // a non-finite S moves no controller state, but the sync took
-                // place: Algorithm 2's counter restarts all the same
-                status = ADPSGD_ENONFINITE;
-                st.cnt = 0;
-            }
+            // a non-finite S restarts the counter and moves nothing else
+            if (!apply_sync(r.rule, r.t, r.gamma, tot.a, &st, nullptr)) status = ADPSGD_ENONFINITE;
             st.t = r.t + 1;
             *r.sched = st;
             p_next = st.p;

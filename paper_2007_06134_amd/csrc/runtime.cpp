@@ -815,10 +815,8 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
             if (var_log) std::memcpy(var_log + (size_t)n_done * c->T, var, sizeof(double) * c->T);
         }
         ++n_done;
-        if (rc) {
-            known.cnt = 0;  // the sync took place; only the controller's update is withheld
-            return hdr.status == rc ? rc : fail(ADPSGD_ESTATE, "device and host disagree on a non-finite S");
-        }
+        // (a non-finite S still restarted the counter; only p and C2 stay)
+        if (rc) return hdr.status == rc ? rc : fail(ADPSGD_ESTATE, "device and host disagree on a non-finite S");
         if (hdr.status != ADPSGD_OK || hdr.p_next != known.p || hdr.C2 != known.C2 || hdr.nC2 != known.nC2)
             return fail(ADPSGD_ESTATE, "device and host controllers disagree at step " + std::to_string(e.t));
         return ADPSGD_OK;

@@ -61,12 +61,13 @@ ADPSGD_HD bool sync_decisive(const SchedRule &r, int64_t t) {
 // and gamma step t's rate: the counter restarts; in the sampling phase
 // (t < K_s) C2 becomes the running mean of S / gamma; afterwards p moves by one
 // when S leaves [thr_lo gamma C2, thr_hi gamma C2] (p within [1, p_max]).
-// Returns false, leaving the state untouched, when S is not finite.  margin
-// (may be null): signed relative distance of S to the nearer band edge.
+// The sync took place whatever S is, so the counter restarts (line 9) in
+// every case; a non-finite S then returns false with C2, nC2 and p untouched.
+// margin (may be null): signed relative distance of S to the nearer band edge.
 ADPSGD_HD bool apply_sync(const SchedRule &r, int64_t t, double gamma, double S, SchedState *st, double *margin) {
     if (margin) *margin = __builtin_nan("");
-    if (!__builtin_isfinite(S)) return false;
     st->cnt = 0;
+    if (!__builtin_isfinite(S)) return false;
     if (r.period_mode != ADPSGD_PERIOD_ADAPTIVE || t < r.warmup) return true;
     if (t < r.k_s) {
         st->nC2 += 1;
