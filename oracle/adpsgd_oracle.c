@@ -28,7 +28,7 @@
  *     period is Algorithm 2 without controller updates.
  *   - Momentum buffers are not averaged by default; only the parameters are
  *     (avg_momentum = 1 averages them too, the other reading).
- *   - p never drops below 1.
+ *   - p never drops below 1 and, when a cap p_max is given, never exceeds it.
  *   - The variance divides by K (not K-1) and sums over parameters.
  *
  * The paper's other strategies, as options of the same loop:
@@ -156,7 +156,7 @@ typedef struct {
     int64_t sync_warmup_steps; /* steps before this one sync every step, no controller */
     int64_t p_switch_step;     /* constant modes: period p_after from this step on (0: never) */
     int32_t p_after;
-    int32_t pad_;
+    int32_t p_max;             /* upper bound on the adaptive period; 0: none */
 } orc_problem;
 
 typedef struct {
@@ -371,6 +371,8 @@ double orc_grad_norm2(const orc_problem *pb, int64_t n, const double *x, const d
 /* Period controller after a sync at step t with variance S (Algorithm 2,
  * lines 13-19).  Inactive in the constant modes and during the warm-up prefix
  * (there the run synchronizes every step and Algorithm 2 has not started).
+ * The period stays within [1, p_max]: line 19 would reach 0, and the paper
+ * gives no upper bound, so one is an option (p_max = 0: none).
  * Returns 0, or -4 if S is not finite (state unchanged). */
 int orc_controller(const orc_problem *pb, orc_state *st, int64_t t, double S)
 {
@@ -382,7 +384,7 @@ int orc_controller(const orc_problem *pb, orc_state *st, int64_t t, double S)
         st->nC2 += 1;
         st->C2 += (S / gamma - st->C2) / (double)st->nC2;
     } else if (S < pb->thr_lo * gamma * st->C2) {
-        st->p += 1;
+        if (pb->p_max <= 0 || st->p < pb->p_max) st->p += 1;
     } else if (S > pb->thr_hi * gamma * st->C2) {
         if (st->p > 1) st->p -= 1;
     }

@@ -47,7 +47,7 @@ class _Problem(C.Structure):
         ("thr_lo", C.c_double), ("thr_hi", C.c_double),
         ("p_init", C.c_int32), ("avg_momentum", C.c_int32),
         ("sync_warmup_steps", C.c_int64), ("p_switch_step", C.c_int64),
-        ("p_after", C.c_int32), ("pad_", C.c_int32),
+        ("p_after", C.c_int32), ("p_max", C.c_int32),
     ]
 
 
@@ -179,7 +179,7 @@ class Oracle:
             lr0=w.lr0, total_steps=w.total_steps, k_s=w.k_s, thr_lo=w.thr_lo,
             thr_hi=w.thr_hi, p_init=w.p_init, avg_momentum=1 if w.avg_momentum else 0,
             sync_warmup_steps=w.sync_warmup_steps, p_switch_step=w.p_switch_step,
-            p_after=w.p_after, pad_=0)
+            p_after=w.p_after, p_max=w.p_max)
         self.lib = _load()
 
     def lr(self, t: int) -> float:
@@ -294,20 +294,31 @@ def lr(w, t: int) -> float:
     return Oracle(w).lr(t)
 
 
-def controller_trace(w, S_of_sync):
+def controller_trace(w, S_of_sync, through_nonfinite: bool = False):
     """Drive the oracle's schedule with scripted variances.
 
     S_of_sync(t, gamma) gives S for a sync after step t.  Returns the list of
-    (t, p in force) syncs over w.total_steps steps and the final state.
+    (t, p in force) syncs over w.total_steps steps and the final state.  A
+    non-finite S stops the oracle's schedule at that sync (with its counter
+    restarted); through_nonfinite=True then resumes it from the state it left,
+    else FloatingPointError is raised.
     """
     o = Oracle(w)
     st = o.new_state()
     N = w.total_steps
     S = np.array([float(S_of_sync(t, o.lr(t))) for t in range(N)])
-    sync_t = np.zeros(N, dtype=np.int64)
-    sync_p = np.zeros(N, dtype=np.int32)
-    n = o.lib.orc_schedule_trace(C.byref(o.pb), C.byref(st), N, _dp(S), _ip(sync_t),
-                                 sync_p.ctypes.data_as(C.POINTER(C.c_int32)), N)
-    if n < 0:
-        raise FloatingPointError(n)
-    return [(int(a), int(b)) for a, b in zip(sync_t[:n], sync_p[:n])], st
+    out = []
+    while st.t < N:
+        left = N - st.t
+        sync_t = np.full(left, -1, dtype=np.int64)
+        sync_p = np.zeros(left, dtype=np.int32)
+        n = o.lib.orc_schedule_trace(C.byref(o.pb), C.byref(st), left, _dp(S), _ip(sync_t),
+                                     sync_p.ctypes.data_as(C.POINTER(C.c_int32)), left)
+        if n >= 0:
+            out += [(int(a), int(b)) for a, b in zip(sync_t[:n], sync_p[:n])]
+            break
+        if not through_nonfinite:
+            raise FloatingPointError(n)
+        k = int(np.count_nonzero(sync_t >= 0))   # syncs recorded up to the failing one
+        out += [(int(a), int(b)) for a, b in zip(sync_t[:k], sync_p[:k])]
+    return out, st

@@ -32,7 +32,7 @@ def hparams_of(w) -> adpsgd_hparams:
                         k_s=w.k_s, thr_lo=w.thr_lo, thr_hi=w.thr_hi,
                         sync_warmup_steps=getattr(w, "sync_warmup_steps", 0),
                         p_switch_step=getattr(w, "p_switch_step", 0), p_after=getattr(w, "p_after", 0),
-                        avg_momentum=getattr(w, "avg_momentum", False))
+                        avg_momentum=getattr(w, "avg_momentum", False), p_max=getattr(w, "p_max", 0))
 
 
 class Adpsgd:

@@ -38,6 +38,7 @@ static int one(int32_t K, const int64_t *off, int32_t T, int32_t mode, int32_t a
     pb.sync_warmup_steps = warm;
     pb.p_switch_step = switch_step;
     pb.p_after = p_after;
+    pb.p_max = (mode == 1 && steps % 2) ? 4 : 0;   /* a cap on the adaptive period in some runs */
     const int64_t P = pb.P;
 
     double *h = NEW(double, P), *xs = NEW(double, P);

@@ -116,6 +116,20 @@ def test_controller_matches_oracle_on_random_variances(A, seed):
     assert len({p for _, p in lib}) > 3
 
 
+@pytest.mark.parametrize("p_max", [3, 5, 9])
+def test_controller_cap_matches_oracle(A, p_max):
+    """The library's bound on p (p within [1, p_max]) against the oracle's, on
+    variances that shrink after the sampling phase so the period keeps growing."""
+    w = W.full_workloads()["resnet18_like"].replace(total_steps=3000, k_s=600, p_init=3, p_max=p_max)
+    rng = np.random.default_rng(p_max)
+    noise = rng.lognormal(0.0, 0.3, size=4000)
+    S_fn = lambda t, g: float(noise[t] * g * (1.0 if t < 600 else 0.5 + 0.4 * math.cos(t / 200.0)))
+    lib, st_l = _lib_trace(A, w, S_fn)
+    orc, st_o = oracle.controller_trace(w, S_fn)
+    assert lib == orc
+    assert max(p for _, p in lib) == p_max and st_l.p == st_o.p
+
+
 def test_controller_scripted_cases(A):
     w = W.full_workloads()["resnet50_like"].replace(total_steps=400, k_s=100, p_init=4,
                                                     lr_kind=W.LR_CONST)
@@ -152,10 +166,43 @@ def test_controller_non_finite_keeps_state(A):
     st = A.adpsgd_sched_init(hp)
     st.p, st.C2, st.nC2 = 7, 2.0, 3
     for bad in (float("nan"), float("inf"), -float("inf")):
+        st.cnt = 5
         with pytest.raises(A.AdpsgdError) as e:
             A.adpsgd_sched_on_sync(hp, st, 500, bad)
         assert e.value.code == A.ENONFINITE
-        assert (st.p, st.C2, st.nC2) == (7, 2.0, 3)
+        # the sync took place: the counter restarts; nothing else moves
+        assert (st.p, st.C2, st.nC2, st.cnt) == (7, 2.0, 3, 0)
+
+
+@pytest.mark.parametrize("bad_syncs", [(0,), (3, 40), (7, 8, 9)])
+def test_controller_through_non_finite_matches_oracle(A, bad_syncs):
+    """A host-only controller driven through syncs whose S is NaN keeps syncing
+    every p steps afterwards, as the oracle's schedule does (Algorithm 2, line
+    9 restarts the counter at every sync)."""
+    w = W.full_workloads()["resnet50_like"].replace(total_steps=600, k_s=100, p_init=3)
+    rng = np.random.default_rng(len(bad_syncs))
+    noise = rng.lognormal(0.0, 0.4, size=600)
+    S_ok = lambda t, g: float(noise[t] * g)
+    orc_first, _ = oracle.controller_trace(w, S_ok)
+    bad_t = {orc_first[j][0] for j in bad_syncs}
+    S_fn = lambda t, g: float("nan") if t in bad_t else S_ok(t, g)
+    hp = A.hparams_of(w)
+    st = A.adpsgd_sched_init(hp)
+    lib, n_bad = [], 0
+    for t in range(w.total_steps):
+        if A.adpsgd_sched_step(hp, st):
+            lib.append((t, st.p))
+            try:
+                A.adpsgd_sched_on_sync(hp, st, t, S_fn(t, A.adpsgd_lr(hp, t)))
+            except A.AdpsgdError as e:
+                assert e.code == A.ENONFINITE
+                n_bad += 1
+            assert st.cnt == 0
+    orc, st_o = oracle.controller_trace(w, S_fn, through_nonfinite=True)
+    assert n_bad == len(bad_t)
+    assert lib == orc
+    assert (st.p, st.nC2, st.cnt) == (st_o.p, st_o.nC2, st_o.cnt)
+    assert st.C2 == pytest.approx(st_o.C2, rel=1e-12)
 
 
 def test_constant_mode_never_changes_period(A):

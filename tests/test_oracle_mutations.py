@@ -63,6 +63,10 @@ MUTATIONS = [
      "if (st->p > 1) st->p -= 1;",
      "st->p -= 1;",
      "test_controller_huge_variance_clamps_period_at_one"),
+    ("period growth ignores the cap",
+     "if (pb->p_max <= 0 || st->p < pb->p_max) st->p += 1;",
+     "st->p += 1;",
+     "test_controller_period_cap"),
     ("sync one step late",
      "return st->cnt >= st->p;",
      "return st->cnt > st->p;",

@@ -190,6 +190,24 @@ def test_controller_huge_variance_clamps_period_at_one():
     assert st.p == 1
 
 
+def test_controller_period_cap():
+    """p stays within [1, p_max] (the reading of lines 16-19 with an upper bound):
+    zero variance after sampling grows p by one per sync until the cap, then the
+    period stays; a cap equal to p_init fixes the period; no cap grows on."""
+    w = _adaptive()
+    S_fn = lambda t, g: (1.0 * g if t < 100 else 0.0)
+    syncs, st = oracle.controller_trace(w.replace(p_max=7), S_fn)
+    after = [p for t, p in syncs if t >= 100]
+    assert after[:6] == [4, 5, 6, 7, 7, 7] and set(after[3:]) == {7} and st.p == 7
+    syncs, st = oracle.controller_trace(w.replace(p_max=4), S_fn)
+    assert {p for _, p in syncs} == {4} and len(syncs) == w.total_steps // 4
+    syncs, st = oracle.controller_trace(w, S_fn)
+    assert st.p > 7
+    # the cap does not hold p down when the variance asks for less
+    syncs, st = oracle.controller_trace(w.replace(p_max=5), lambda t, g: (1.0 * g if t < 100 else 1e9))
+    assert [p for t, p in syncs if t >= 100][:4] == [4, 3, 2, 1]
+
+
 def test_controller_band_keeps_period():
     w = _adaptive()
     # S/gamma == C2 exactly, also across thresholds 0.7..1.3 (strict comparisons)

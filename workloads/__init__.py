@@ -54,6 +54,7 @@ class Workload:
     p_switch_step: int = 0       # constant modes: the period becomes p_after from this step
     p_after: int = 0
     avg_momentum: bool = False   # average the momentum buffers at a sync as well
+    p_max: int = 0               # upper bound on the adaptive period (0: none)
 
     @property
     def P(self) -> int:
