@@ -3,8 +3,10 @@
 Argument marshalling only: every step of the hot path runs in the library's
 HIP kernels.  Functions keep the C names; a failing status raises
 ``AdpsgdError`` carrying the library's message.  If the library has not been
-built, importing this module builds it (hipcc, gfx950); if that fails it
-raises ImportError (there is no fallback).
+built, or was built from other sources than those in the tree (a digest
+recorded at build time), importing this module builds it (hipcc, gfx950); if
+that fails, or ADPSGD_NO_REBUILD is set, it raises ImportError (there is no
+fallback).
 """
 from __future__ import annotations
 
@@ -72,14 +74,23 @@ class adpsgd_timing(C.Structure):
                 ("trace_ms", C.c_double), ("trace_launches", C.c_int64)]
 
 
-if not os.path.exists(LIB_PATH):
-    # nothing built yet: build it now with hipcc (gfx950); if that fails there is
-    # no library and no fallback
+from . import build as _build  # noqa: E402
+
+if not _build.is_current():
+    # nothing built yet, or built from other sources than the ones here (the
+    # digest written next to the library at build time differs): build it now
+    # with hipcc (gfx950).  ADPSGD_NO_REBUILD=1 refuses instead.  There is no
+    # fallback either way.
+    _why = "is not built" if not os.path.exists(LIB_PATH) else "was built from other sources"
+    if os.environ.get("ADPSGD_NO_REBUILD"):
+        raise ImportError(f"{LIB_PATH} {_why} (source digest differs) and ADPSGD_NO_REBUILD is set; "
+                          "run `python -m paper_2007_06134_amd.build`")
+    import sys as _sys
+    print(f"paper_2007_06134_amd: {LIB_PATH} {_why}; building it", file=_sys.stderr, flush=True)
     try:
-        from . import build as _build
         _build.build()
     except Exception as e:  # noqa: BLE001
-        raise ImportError(f"{LIB_PATH} is not built and building it failed ({e}); "
+        raise ImportError(f"{LIB_PATH} {_why} and building it failed ({e}); "
                           "run `python -m paper_2007_06134_amd.build`") from e
 
 # One HIP runtime per process.  torch ships its own libamdhip64 and finds it

@@ -4,6 +4,7 @@ Usage: ``python -m paper_2007_06134_amd.build`` (or ``build()`` from Python).
 """
 from __future__ import annotations
 
+import hashlib
 import os
 import shutil
 import subprocess
@@ -18,8 +19,40 @@ LIB = os.path.join(PKG, "libadpsgd.so")
 ARCH = "gfx950"
 ROCM_LIB = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "lib")   # roctx markers
 
+DIGEST = LIB + ".digest"   # source digest of the library next to it
+
 HIP_SOURCES = ["kernels.hip"]
 HOST_SOURCES = ["runtime.cpp", "controller.cpp"]
+
+
+def source_digest() -> str:
+    """sha256 over every file the library is built from: the sources under
+    csrc/, the headers under include/ and this build script (its flags)."""
+    h = hashlib.sha256()
+    files = [os.path.join(CSRC, f) for f in sorted(os.listdir(CSRC))]
+    files += [os.path.join(INCLUDE, f) for f in sorted(os.listdir(INCLUDE))]
+    files.append(os.path.abspath(__file__))
+    for path in files:
+        if not os.path.isfile(path):
+            continue
+        h.update(os.path.relpath(path, ROOT).encode() + b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()
+
+
+def built_digest() -> str:
+    """The source digest recorded when the library was last built ('' if none)."""
+    try:
+        with open(DIGEST) as f:
+            return f.read().strip()
+    except OSError:
+        return ""
+
+
+def is_current() -> bool:
+    return os.path.exists(LIB) and built_digest() == source_digest()
 
 # Packed fp32 instructions are kept out of the device code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
@@ -35,6 +68,7 @@ def hipcc() -> str:
 
 def build(verbose: bool = False) -> str:
     cc = hipcc()
+    digest = source_digest()
     with tempfile.TemporaryDirectory(prefix="adpsgd_build_") as tmp:
         objs = []
         for src in HIP_SOURCES:
@@ -53,6 +87,10 @@ def build(verbose: bool = False) -> str:
         _run([cc, "-shared", f"--offload-arch={ARCH}", *objs, "-L", ROCM_LIB, "-lrocprofiler-sdk-roctx",
               f"-Wl,-rpath,{ROCM_LIB}", "-o", out_tmp], verbose)
         os.replace(out_tmp, LIB)
+    tmp_digest = DIGEST + f".tmp{os.getpid()}"
+    with open(tmp_digest, "w") as f:
+        f.write(digest + "\n")
+    os.replace(tmp_digest, DIGEST)
     return LIB
 
 
