@@ -16,7 +16,7 @@ import pytest
 import oracle
 import oracle.oracle as OO
 import workloads as W
-from helpers import max_rel_err, rel_err
+from helpers import MOM_FLOOR, MOM_TOL, PARAM_TOL, max_rel_err, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -161,8 +161,8 @@ def test_random_call_sequence_matches_oracle(A, i):
         x = eng.x.double().cpu().numpy()
         m = eng.m.double().cpu().numpy()
     _say(f"calls {i}: K={w.K} P={w.P} mode={w.period_mode}: {' '.join(ops)}")
-    assert max_rel_err(x, ref.x, w.offsets()) < 1e-4
-    assert max_rel_err(m, ref.v, w.offsets(), floor=1.0) < 1e-3
+    assert max_rel_err(x, ref.x, w.offsets()) < PARAM_TOL
+    assert max_rel_err(m, ref.v, w.offsets(), floor=MOM_FLOOR) < MOM_TOL
 
 
 def test_period_switch_applies_to_the_state_of_manual_calls(A):
