@@ -206,7 +206,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "K": w.K, "P": w.P, "T": w.T, "local_steps_per_run": N,
                    "period": period_text(w),
-                   "syncs_per_run": int(n_syncs[-1])},
+                   "syncs_per_run": int(n_syncs[-1]),
+                   # the periods the controller chose in the last timed run
+                   "p_range": [int(recs["p"].min()), int(recs["p"].max())] if len(recs) else None},
     }
     if args.traced:
         out["config"]["mode"] = "traced"
@@ -216,8 +218,16 @@ def main():
     if tm.step_launches > 0:
         step_ms = tm.step_ms / tm.step_launches
         achieved = step_bytes / (step_ms * 1e-3) / 1e9
+        traffic = measured_traffic(w, step_block, step_lds, step_row_chunks)
         out["roofline"] = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(w, step_block, step_lds, step_row_chunks),
+                           "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                           # traffic is not measured in this run: it is the copy-scaled
+                           # FETCH_SIZE + WRITE_SIZE of a separate rocprofv3 --pmc run,
+                           # read from the committed summary when it was taken on these
+                           # kernel sources and this launch shape (else null)
+                           "traffic_source": {"profile": os.path.relpath(TRAFFIC_FILE, ROOT),
+                                              "kernel_sources_digest": kernel_source_digest(),
+                                              "matched": traffic is not None},
                            "kernel": f"k_local_step<{step_block}>",
                            "lds_reserved_per_block": step_lds, "row_chunks": step_row_chunks,
                            "row_stride": row_stride,
