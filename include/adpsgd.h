@@ -79,7 +79,12 @@ extern "C" {
 #define ADPSGD_LAUNCH_HYBRID 0  /* default: steps the host can plan run as plain steps or
                                    fused syncs; after a decisive sync the host waits for
                                    its outcome while the GPU has queued work, else the
-                                   device decides the next steps itself                  */
+                                   device decides the next steps itself.  A run in a
+                                   constant-period mode on a problem of K * P < 2^24
+                                   (launch-bound) and up to 65536 steps, with timing off,
+                                   is captured once as a HIP graph of the same launches and
+                                   replayed while runs repeat with the same start state,
+                                   length and step launch shape                            */
 #define ADPSGD_LAUNCH_DEVICE 1  /* every step is decided on the device (step + optional
                                    sync + reduction per step)                              */
 #define ADPSGD_LAUNCH_HOST 2    /* the host waits for every decision it needs; the device
@@ -187,6 +192,8 @@ typedef struct {
     double segsum_ms;   int64_t segsum_launches;   /* reduction: per-tensor sums and,
                                                       in a run, the period decision */
     double trace_ms;    int64_t trace_launches;    /* traced plain step (step + variance) */
+    int64_t graph_captures;  /* runs captured as a HIP graph (ADPSGD_LAUNCH_HYBRID), and */
+    int64_t graph_replays;   /* runs replayed from one; counted whether timing is on or off */
 } adpsgd_timing;
 
 /* Bytes of device workspace for K workers, P parameters and T tensors with
@@ -245,7 +252,11 @@ ADPSGD_API int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
  * forced at the end.  Returns when all enqueued work has finished.  On
  * ENONFINITE the run stops at that sync, whose update of p and C2 is withheld
  * (its counter restarts, as at every sync); steps already enqueued after it
- * complete (with their syncs, logged) and are counted in the state. */
+ * complete (with their syncs, logged) and are counted in the state (a run
+ * replayed as a graph has enqueued all its steps).  The graph of a
+ * constant-period run (ADPSGD_LAUNCH_HYBRID) is captured on a stream of the
+ * library's own and launched on the context's stream; it holds pinned record
+ * slots, one per sync, until the context is destroyed. */
 ADPSGD_API int adpsgd_run(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_t log_cap,
                double *var_log, int64_t *n_syncs);
 

@@ -71,7 +71,8 @@ class adpsgd_timing(C.Structure):
                 ("fused_ms", C.c_double), ("fused_launches", C.c_int64),
                 ("average_ms", C.c_double), ("average_launches", C.c_int64),
                 ("segsum_ms", C.c_double), ("segsum_launches", C.c_int64),
-                ("trace_ms", C.c_double), ("trace_launches", C.c_int64)]
+                ("trace_ms", C.c_double), ("trace_launches", C.c_int64),
+                ("graph_captures", C.c_int64), ("graph_replays", C.c_int64)]
 
 
 from . import build as _build  # noqa: E402

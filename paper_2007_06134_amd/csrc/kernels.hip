@@ -91,24 +91,25 @@ __device__ __forceinline__ void sgd_update(const StepParams &a, f4 &x, f4 &m, f4
 }
 
 // Sums of a pair of values over the block in a fixed order: wave64 butterfly,
-// then the waves in order.  Valid on thread 0.
+// then the waves in order.  Valid on thread 0.  TWO = false: b is known to be
+// zero everywhere (no gradient norm outside tracing) and is not reduced.
 struct Pair {
     double a, b;
 };
-template <int WAVES>
+template <int WAVES, bool TWO = true>
 __device__ __forceinline__ Pair block_sum2(double a, double b) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         a += __shfl_xor(a, off, 64);
-        b += __shfl_xor(b, off, 64);
+        if (TWO) b += __shfl_xor(b, off, 64);
     }
     if constexpr (WAVES == 1) {
-        return Pair{a, b};
+        return Pair{a, TWO ? b : 0.0};
     } else {
-        __shared__ double wave_a[WAVES], wave_b[WAVES];
+        __shared__ double wave_a[WAVES], wave_b[TWO ? WAVES : 1];
         if ((threadIdx.x & 63) == 0) {
             wave_a[threadIdx.x >> 6] = a;
-            wave_b[threadIdx.x >> 6] = b;
+            if (TWO) wave_b[threadIdx.x >> 6] = b;
         }
         __syncthreads();
         Pair total{0.0, 0.0};
@@ -116,7 +117,7 @@ __device__ __forceinline__ Pair block_sum2(double a, double b) {
 #pragma unroll
             for (int w = 0; w < WAVES; ++w) {
                 total.a += wave_a[w];
-                total.b += wave_b[w];
+                if (TWO) total.b += wave_b[w];
             }
         }
         return total;
@@ -235,7 +236,11 @@ __device__ __forceinline__ f4 tree_sum_lds_n(const f4 (*rows)[64], int lane, int
 template <int KT, int WC, int RD>
 __device__ __forceinline__ f4 lds_mean(const f4 (*rows)[64], int lane, int W, int K) {
     if constexpr (KT > 0) {
-        return tree_sum_lds<WC>(rows, lane, 0) / splat((float)KT);
+        // every compiled K is a power of two: the product by 1/K is the
+        // correctly rounded quotient, the same bits as the division, at a
+        // fraction of its instructions
+        static_assert((KT & (KT - 1)) == 0, "compiled worker counts are powers of two");
+        return tree_sum_lds<WC>(rows, lane, 0) * splat(1.0f / (float)KT);
     } else if constexpr (RD > 1) {
         return tree_sum_lds_n(rows, lane, W) / splat((float)K);
     } else {
@@ -288,23 +293,24 @@ constexpr int sync_waves() {
 }
 
 // block_sum2 over a run-time number of waves (at most 16), in the same order.
+template <bool TWO = true>
 __device__ __forceinline__ Pair block_sum2_waves(double a, double b, int waves) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) {
         a += __shfl_xor(a, off, 64);
-        b += __shfl_xor(b, off, 64);
+        if (TWO) b += __shfl_xor(b, off, 64);
     }
-    __shared__ double wave_a[16], wave_b[16];
+    __shared__ double wave_a[16], wave_b[TWO ? 16 : 1];
     if ((threadIdx.x & 63) == 0) {
         wave_a[threadIdx.x >> 6] = a;
-        wave_b[threadIdx.x >> 6] = b;
+        if (TWO) wave_b[threadIdx.x >> 6] = b;
     }
     __syncthreads();
     Pair total{0.0, 0.0};
     if (threadIdx.x == 0)
         for (int w = 0; w < waves; ++w) {
             total.a += wave_a[w];
-            total.b += wave_b[w];
+            if (TWO) total.b += wave_b[w];
         }
     return total;
 }
@@ -411,8 +417,8 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         if (GN && w == 0) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
     }
     Pair total;
-    if constexpr (KT > 0) total = block_sum2<WMAX>(acc, gn);
-    else total = block_sum2_waves(acc, gn, W);
+    if constexpr (KT > 0) total = block_sum2<WMAX, GN>(acc, gn);
+    else total = block_sum2_waves<GN>(acc, gn, W);
     if (threadIdx.x == 0) {
         p.partials[2 * ti] = total.a;
         p.partials[2 * ti + 1] = total.b;
@@ -483,7 +489,7 @@ __global__ void __launch_bounds__(64) k_sync_loop(SyncParams p) {
         }
     }
     if (!measure) return;
-    const Pair total = block_sum2<1>(acc, gn);
+    const Pair total = block_sum2<1, GN>(acc, gn);
     if (threadIdx.x == 0) {
         p.partials[2 * ti] = total.a;
         p.partials[2 * ti + 1] = total.b;
@@ -852,8 +858,11 @@ constexpr int any_k_waves(int K) { return (K + any_k_rows(K) - 1) / any_k_rows(K
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD, bool RAGGED>
 hipError_t sync_variant(const SyncParams &p, int64_t n_tiles, int cap, hipStream_t st) {
     const int threads = KT > 0 ? 64 * sync_waves<KT, MODE>() : 64 * any_k_waves(p.s.K);
-    static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED>);
-    const int lds = cap_lds(cap, own);
+    int lds = 0;
+    if (cap > 0) {   // (the attribute query only when it is needed: not under graph capture)
+        static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED>);
+        lds = cap_lds(cap, own);
+    }
     return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
         SyncParams q = p;
         q.s.block0 = b0;

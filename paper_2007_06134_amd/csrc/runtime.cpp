@@ -79,6 +79,12 @@ constexpr int64_t kPollEvery = 8;
 // adpsgd_init times the local step's block sizes when one step moves at least
 // this many elements (below it a launch is too short to time reliably).
 constexpr double kTuneMinElems = 16.0 * 1024 * 1024;
+// Below the same size a step takes a few microseconds on the GPU, less than
+// the host needs to launch it, so runs whose schedule is known in advance
+// (the constant-period modes) are captured once as a HIP graph and replayed;
+// runs of up to kGraphMaxSteps steps.
+constexpr double kGraphMaxElems = kTuneMinElems;
+constexpr int64_t kGraphMaxSteps = int64_t(1) << 16;
 constexpr int64_t kMaxK = 65536;
 constexpr int64_t kMaxCounter = int64_t(1) << 32;  // Philox counter words are 32-bit
 
@@ -246,12 +252,33 @@ struct adpsgd_ctx {
     std::vector<hipEvent_t> ev_pool;
     double t_ms[tKinds] = {};
     int64_t t_n[tKinds] = {};
+    // A constant-period run captured as a HIP graph (run_impl): captured on a
+    // private non-blocking stream, launched on the context's stream, kept for
+    // as long as runs repeat with the same start state, length and launch shape.
+    hipStream_t cap_stream = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t graph_exec = nullptr;
+    int64_t graph_key[7] = {};
+    int64_t graph_captures = 0, graph_replays = 0;   // since the last adpsgd_set_timing
+    char *h_gslots = nullptr;       // one record slot per sync of the captured run (pinned)
+    char *d_gslots = nullptr;
+    int64_t gslot_cap = 0;
 };
 
 namespace {
 
+void drop_graph(adpsgd_ctx *c) {
+    if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
+    if (c->graph) (void)hipGraphDestroy(c->graph);
+    c->graph_exec = nullptr;
+    c->graph = nullptr;
+}
+
 void release(adpsgd_ctx *c) {
     if (!c) return;
+    drop_graph(c);
+    if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+    if (c->h_gslots) (void)hipHostFree(c->h_gslots);
     for (auto &ev : c->ring_ev)
         if (ev) (void)hipEventDestroy(ev);
     for (auto &tl : c->timed) {
@@ -383,23 +410,9 @@ SyncParams sync_params(const adpsgd_ctx *c, int64_t t) {
 char *slot_dev(const adpsgd_ctx *c, int slot) { return c->d_slots + (size_t)slot * c->slot_bytes; }
 const char *slot_host(const adpsgd_ctx *c, int slot) { return c->h_slots + (size_t)slot * c->slot_bytes; }
 
-// The sync-tile kernel of the given mode at step t, then the reduction into
-// record slot `slot` (with the controller on the device when ctl), then the
-// slot's event.  *step_seq: the timed sequence number of the tile kernel (its
-// kind is open for the device-decided modes).
-int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t *step_seq) {
-    const bool dev = mode == kDevice || mode == kDeviceTrace;
-    const SyncParams sp = sync_params(c, t);
-    const int64_t n_tiles = (int64_t)c->tiles.size();
-    const int kind = dev ? -1 : mode == kAverage ? tAverage : tFused;
-    int rc = timed_launch(
-        c, kind,
-        [&] {
-            return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
-                                    mode == kAverage ? c->average_cap : 0, c->stream);
-        },
-        step_seq);
-    if (rc) return rc;
+// The reduction after a sync-tile kernel at step t, writing its record to the
+// slot at device address `slot` (with the controller on the device when ctl).
+ReduceParams reduce_params(const adpsgd_ctx *c, int mode, int64_t t, char *slot, bool ctl) {
     ReduceParams r;
     r.tile_partials = c->d_tile_partials;
     r.chunks = c->d_chunks;
@@ -417,16 +430,84 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     r.win_partials = c->d_win_partials;
     r.n_windows = c->win_begin.empty() ? 0 : (int32_t)c->win_begin.size() - 1;
     r.pad2_ = 0;
-    r.hdr = reinterpret_cast<SlotHdr *>(slot_dev(c, slot));
-    r.out = reinterpret_cast<double *>(slot_dev(c, slot) + kSlotHdrBytes);
+    r.hdr = reinterpret_cast<SlotHdr *>(slot);
+    r.out = reinterpret_cast<double *>(slot + kSlotHdrBytes);
     r.sched = ctl ? c->d_sched : nullptr;
-    r.rule = sp.rule;
+    r.rule = rule_of(&c->hp);
     r.t = t;
     r.gamma = adpsgd_lr(&c->hp, t);
     r.traced = mode == kDeviceTrace ? 1 : 0;
+    return r;
+}
+
+// The sync-tile kernel of the given mode at step t, then the reduction into
+// record slot `slot` (with the controller on the device when ctl), then the
+// slot's event.  *step_seq: the timed sequence number of the tile kernel (its
+// kind is open for the device-decided modes).
+int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t *step_seq) {
+    const bool dev = mode == kDevice || mode == kDeviceTrace;
+    const SyncParams sp = sync_params(c, t);
+    const int64_t n_tiles = (int64_t)c->tiles.size();
+    const int kind = dev ? -1 : mode == kAverage ? tAverage : tFused;
+    int rc = timed_launch(
+        c, kind,
+        [&] {
+            return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
+                                    mode == kAverage ? c->average_cap : 0, c->stream);
+        },
+        step_seq);
+    if (rc) return rc;
+    const ReduceParams r = reduce_params(c, mode, t, slot_dev(c, slot), ctl);
     rc = timed_launch(c, tSegsum, [&] { return launch_reduce(r, c->stream); });
     if (rc) return rc;
     HIP_TRY(hipEventRecord(c->ring_ev[slot], c->stream));
+    return ok();
+}
+
+// Capture steps t0 .. t0 + due.size() - 1 as a graph, launched as the eager
+// driver launches a schedule it knows in advance: plain steps, and for the
+// j-th sync the fused step + sync and the reduction (controller on the device)
+// into the j-th graph record slot.  No events: records are read after the
+// whole graph has run.
+int capture_run(adpsgd_ctx *c, int64_t t0, const std::vector<char> &due, int64_t n_sync) {
+    drop_graph(c);
+    if (n_sync > c->gslot_cap) {
+        if (c->h_gslots) (void)hipHostFree(c->h_gslots);
+        c->h_gslots = c->d_gslots = nullptr;
+        c->gslot_cap = 0;
+        HIP_TRY(hipHostMalloc((void **)&c->h_gslots, (size_t)n_sync * c->slot_bytes,
+                              hipHostMallocMapped | hipHostMallocCoherent));
+        HIP_TRY(hipHostGetDevicePointer((void **)&c->d_gslots, c->h_gslots, 0));
+        c->gslot_cap = n_sync;
+    }
+    if (!c->cap_stream) HIP_TRY(hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking));
+    const hipStream_t cs = c->cap_stream;
+    const int64_t n_tiles = (int64_t)c->tiles.size();
+    HIP_TRY(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal));
+    hipError_t e = hipSuccess;
+    int64_t j = 0;
+    for (size_t i = 0; i < due.size() && e == hipSuccess; ++i) {
+        const int64_t t = t0 + (int64_t)i;
+        if (!due[i]) {
+            e = launch_local_step(step_params(c, t), c->vec, c->nontemporal, c->step_shape, cs);
+        } else {
+            e = launch_tile_sync(sync_params(c, t), n_tiles, kFused, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
+                                 0, cs);
+            if (e == hipSuccess)
+                e = launch_reduce(reduce_params(c, kFused, t, c->d_gslots + (size_t)j * c->slot_bytes, true), cs);
+            ++j;
+        }
+    }
+    hipGraph_t g = nullptr;
+    const hipError_t e_end = hipStreamEndCapture(cs, &g);
+    if (e == hipSuccess) e = e_end;
+    if (e == hipSuccess) e = hipGraphInstantiate(&c->graph_exec, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        c->graph_exec = nullptr;
+        return hip_fail(e, "capture the run as a HIP graph");
+    }
+    c->graph = g;
     return ok();
 }
 
@@ -779,6 +860,15 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
         return cDue;
     };
 
+    // A run whose schedule is fixed in advance (constant-period modes) on a
+    // small, launch-bound problem replays a captured graph of the whole run.
+    const bool graph_mode = c->policy == ADPSGD_LAUNCH_HYBRID && !traced && !c->timing && n_steps > 0 &&
+                            n_steps <= kGraphMaxSteps && hp.period_mode != ADPSGD_PERIOD_ADAPTIVE &&
+                            (double)c->K * (double)c->P < kGraphMaxElems;
+    auto slot_rec = [&](int slot) -> const char * {
+        return graph_mode ? c->h_gslots + (size_t)slot * c->slot_bytes : slot_host(c, slot);
+    };
+
     struct Entry { int64_t t; bool dev, uncertain; int slot; int64_t seq; };
     std::deque<Entry> inflight;
     adpsgd_state known = c->st;   // the host controller after every accounted step
@@ -798,8 +888,8 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
             return ADPSGD_OK;
         }
         SlotHdr hdr;
-        std::memcpy(&hdr, slot_host(c, e.slot), sizeof hdr);
-        const double *var = reinterpret_cast<const double *>(slot_host(c, e.slot) + kSlotHdrBytes);
+        std::memcpy(&hdr, slot_rec(e.slot), sizeof hdr);
+        const double *var = reinterpret_cast<const double *>(slot_rec(e.slot) + kSlotHdrBytes);
         if (hdr.t != e.t || hdr.due != due)
             return fail(ADPSGD_ESTATE, "device and host schedules disagree at step " + std::to_string(e.t));
         set_timed_kind(c, e.seq, due ? tFused : traced ? tTrace : tStep);
@@ -853,6 +943,41 @@ static int run_impl(adpsgd_ctx *c, int64_t n_steps, adpsgd_sync_rec *log, int64_
     if (n_steps > 0) {
         *c->h_sched = SchedState{known.t, known.cnt, known.nC2, known.C2, known.p, 0};
         HIP_TRY(hipMemcpyAsync(c->d_sched, c->h_sched, sizeof(SchedState), hipMemcpyHostToDevice, c->stream));
+    }
+    if (graph_mode) {
+        // the schedule, from the host controller alone (no decision moves p)
+        std::vector<char> due((size_t)n_steps);
+        adpsgd_state pl = known;
+        int64_t n_sync = 0;
+        for (int64_t j = 0; j < n_steps; ++j) {
+            int32_t d = 0;
+            (void)adpsgd_sched_step(&hp, &pl, &d);
+            due[(size_t)j] = (char)d;
+            if (d) { pl.cnt = 0; ++n_sync; }
+        }
+        const int64_t key[7] = {t0, n_steps, known.cnt, known.p, c->step_shape.block, c->step_shape.lds,
+                                c->step_shape.row_chunks};
+        if (!c->graph_exec || std::memcmp(key, c->graph_key, sizeof key) != 0) {
+            Range cap_("adpsgd_run: capture a graph");
+            if (int rc = capture_run(c, t0, due, n_sync)) return rc;
+            std::memcpy(c->graph_key, key, sizeof key);
+            ++c->graph_captures;
+        }
+        ++c->graph_replays;
+        {
+            Range replay_("adpsgd_run: graph replay");
+            HIP_TRY(hipGraphLaunch(c->graph_exec, c->stream));
+            HIP_TRY(hipStreamSynchronize(c->stream));
+        }
+        int slot = 0;
+        for (int64_t j = 0; j < n_steps; ++j) {
+            const Entry e{t0 + j, due[(size_t)j] != 0, false, due[(size_t)j] ? slot++ : -1, -1};
+            const int rc = account(e);
+            if (rc && status == ADPSGD_OK) status = rc;
+        }
+        c->st = known;
+        if (n_syncs) *n_syncs = n_done;
+        return status != ADPSGD_OK ? status : ok();
     }
     int hard = ADPSGD_OK;  // a HIP failure: stop at once
     while (hard == ADPSGD_OK) {
@@ -963,7 +1088,7 @@ extern "C" int adpsgd_set_step_launch(adpsgd_ctx *c, int32_t block, int32_t lds_
     if (lds_bytes < 0 || lds_bytes > kMaxStepLds) return fail(ADPSGD_EINVAL, "lds_bytes must be in [0, 65536]");
     if (row_chunks < 1 || row_chunks > kMaxRowChunks) return fail(ADPSGD_EINVAL, "row_chunks must be in [1, 4096]");
     c->step_shape = StepShape{block, lds_bytes, row_chunks};
-    return ok();
+    return ok();   // (a captured run keys on the shape, so it is captured again)
 }
 
 extern "C" int adpsgd_get_step_launch(const adpsgd_ctx *c, int32_t *block, int32_t *lds_bytes,
@@ -994,6 +1119,7 @@ extern "C" int adpsgd_set_timing(adpsgd_ctx *c, int32_t every) {
     c->timing_every = every > 0 ? every : 1;
     for (int i = 0; i < tKinds; ++i) { c->t_ms[i] = 0.0; c->t_n[i] = 0; }
     for (auto &n : c->class_count) n = 0;
+    c->graph_captures = c->graph_replays = 0;
     return ok();
 }
 
@@ -1005,7 +1131,7 @@ extern "C" int adpsgd_get_timing(adpsgd_ctx *c, adpsgd_timing *out) {
     if (int rc = harvest(c, true)) return rc;
     *out = adpsgd_timing{c->t_ms[tStep],  c->t_n[tStep],   c->t_ms[tFused],  c->t_n[tFused],
                          c->t_ms[tAverage], c->t_n[tAverage], c->t_ms[tSegsum], c->t_n[tSegsum],
-                         c->t_ms[tTrace], c->t_n[tTrace]};
+                         c->t_ms[tTrace], c->t_n[tTrace], c->graph_captures, c->graph_replays};
     return ok();
 }
 

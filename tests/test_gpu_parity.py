@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
+import oracle.oracle as OO
 import workloads as W
 from helpers import MOM_FLOOR, MOM_TOL, PARAM_TOL, VAR_TOL, assert_same_syncs, gpu_run, max_rel_err, rel_err
 
@@ -310,6 +311,62 @@ def test_launch_policies_agree_bitwise(A, key):
         assert np.array_equal(g["x"], base["x"]) and np.array_equal(g["m"], base["m"]), pol
         assert (g["state"].t, g["state"].cnt, g["state"].p, g["state"].C2) == \
             (base["state"].t, base["state"].cnt, base["state"].p, base["state"].C2), pol
+
+
+def _graph_case(key):
+    pw = W.parity_workloads()
+    return {
+        "quad_small": pw["quad_small"],                       # K = 4, P = 65,536, period 4
+        "vgg16_const8": pw["vgg16_const8"],                   # K = 8, 32 ragged tensors, period 8
+        "alg1_switch": pw["resnet18_like"].replace(           # Algorithm 1's test, a period switch
+            period_mode=W.PERIOD_ALG1, p_init=3, k_s=0, total_steps=300, p_switch_step=150, p_after=7),
+        "warmup_k3": _tiny(K=3, sizes=(5000, 77, 3), total_steps=90, period_mode=W.PERIOD_CONST, p_init=5,
+                           sync_warmup_steps=12),
+    }[key]
+
+
+@pytest.mark.parametrize("key", ["quad_small", "vgg16_const8", "alg1_switch", "warmup_k3"])
+def test_graph_replays_equal_eager_runs(A, key):
+    """A constant-period run of a small problem is captured once as a HIP graph
+    and replayed while the same run repeats.  Every replay, with the program's
+    own eager work and synchronizations between them (single steps, separate
+    syncs, a checkpoint restored), gives the bits of the eager launches of the
+    same run (the host-waiting policy, which never captures)."""
+    import torch
+    w = _graph_case(key)
+    _say(f"graph replays {key}: K={w.K} P={w.P} N={w.total_steps}")
+    ref = gpu_run(w, policy=A.LAUNCH_HOST)
+    with A.Adpsgd.from_workload(w) as eng:
+        for rep in range(4):
+            eng.reset()
+            recs, var, n = eng.run(w.total_steps)
+            assert recs.tobytes() == ref["recs"].tobytes() and np.array_equal(var, ref["var"]), rep
+            assert np.array_equal(eng.x.double().cpu().numpy(), ref["x"]), rep
+            assert np.array_equal(eng.m.double().cpu().numpy(), ref["m"]), rep
+            st = eng.get_state()
+            assert (st.t, st.cnt, st.p) == (ref["state"].t, ref["state"].cnt, ref["state"].p), rep
+            eng.local_steps(3)                       # eager work between the replays
+            eng.average()
+            torch.cuda.synchronize()
+        tm = eng.get_timing()
+        assert (tm.graph_captures, tm.graph_replays) == (1, 4)
+        # another start state is captured again, and matches the oracle
+        eng.reset()
+        eng.local_steps(5)
+        r0 = eng.get_state()
+        recs, var, n = eng.run(40)
+        tm = eng.get_timing()
+        assert (tm.graph_captures, tm.graph_replays) == (2, 5)
+        x = eng.x.double().cpu().numpy()
+    o = oracle.Oracle(w)
+    h, xs = o.problem_data()
+    xo, vo = np.zeros((w.K, w.P)), np.zeros((w.K, w.P))
+    for t in range(5):
+        o.local_step(t, xo, vo, h, xs)
+    ost = OO._State(t=5, cnt=r0.cnt, nC2=0, C2=0.0, p=r0.p)
+    r = o.run(n_steps=40, h=h, xs=xs, x=xo, v=vo, state=ost)
+    assert_same_syncs(recs, r, w)
+    assert max_rel_err(x, r.x, w.offsets()) < PARAM_TOL
 
 
 @pytest.mark.parametrize("key,fused", [("resnet18_like", True), ("many_small", True),
@@ -741,7 +798,7 @@ def _variant(name):
         # an upper bound on p (p within [1, p_max]): p would reach 10 after the
         # LR decays of this run and is held at 3
         "p_max_cap": dict(p_max=3),
-        "p_max_cap_k16": dict(K=16, total_steps=1000, p_init=4, k_s=250, lr_kind=W.LR_COSINE, p_max=6),
+        "p_max_cap_k16": dict(K=16, p_init=4, p_max=6),
     }[name]
     return base.replace(name=name, **v)
 
