@@ -312,6 +312,28 @@ ADPSGD_API int adpsgd_destroy(adpsgd_ctx *c);
 /* Message for the calling thread's last failed call (empty if none). */
 ADPSGD_API const char *adpsgd_last_error(void);
 
+/* ---- synchronization without allocation ------------------------------------ */
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the separate
+ * synchronization of adpsgd_average with no context.  x [K][P] (device, rows
+ * row_stride elements apart, 0 meaning P; 16-byte aligned) is replaced by the
+ * replica mean in every row, and var_out[T] (host) receives the per-tensor
+ * variances (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2 of the replicas
+ * before the mean; tensor_offsets[T+1] (host) as for adpsgd_init.  The
+ * replicas get the same bits as adpsgd_average gives a context of the same
+ * shape; the variances agree to rounding (another summation order).  Blocks
+ * until var_out is valid; runs on `stream` (NULL: the null stream) of the
+ * current device.
+ * It allocates nothing: the tile table, the partial sums and the variances
+ * live in a 64 MiB array of device memory that the library reserves on each
+ * GPU it runs on, for the life of the process (problems of up to about 2
+ * million sync tiles of 256 elements, e.g. 5e8 parameters; larger ones get
+ * EINVAL).  Calls on one GPU share that array: calls that overlap on one GPU
+ * (other threads, other streams) race and must be serialized by the caller. */
+ADPSGD_API int adpsgd_average_noalloc(int32_t K, int64_t P, int64_t row_stride, const int64_t *tensor_offsets,
+                                      int32_t T, float *x, double *var_out, void *stream);
+
 /* ---- generator dumps (the device code the steps use) ------------------------ */
 
 /* dev_out[4j .. 4j+3] = Philox4x32-10(key = (seed mod 2^32, seed >> 32),

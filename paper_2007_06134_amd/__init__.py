@@ -12,7 +12,7 @@ import numpy as np
 
 from ._native import (  # noqa: F401
     AdpsgdError, EDEVICE, EINVAL, ENONFINITE, ESTATE, EXPORTED, LAUNCH_DEVICE, LAUNCH_HOST, LAUNCH_HYBRID,
-    LIB_PATH, LR_CONST, LR_COSINE,
+    LIB_PATH, LR_CONST, LR_COSINE, adpsgd_average_noalloc,
     LR_STEP, LR_WARMUP_STEP, OK, PERIOD_ADAPTIVE, PERIOD_ALG1, PERIOD_CONST, adpsgd_average, adpsgd_buffers, adpsgd_destroy,
     adpsgd_get_state, adpsgd_get_timing, adpsgd_hparams, adpsgd_init, adpsgd_last_error,
     adpsgd_local_steps, adpsgd_lr, adpsgd_normal_dump, adpsgd_philox_dump, adpsgd_reset, adpsgd_run,

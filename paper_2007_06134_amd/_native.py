@@ -128,6 +128,8 @@ _SIGS = {
     "adpsgd_get_timing": (C.c_int, [_CTX, C.POINTER(adpsgd_timing)]),
     "adpsgd_destroy": (C.c_int, [_CTX]),
     "adpsgd_last_error": (C.c_char_p, []),
+    "adpsgd_average_noalloc": (C.c_int, [C.c_int32, C.c_int64, C.c_int64, _I64P, C.c_int32, C.c_void_p, _DP,
+                                         C.c_void_p]),
     "adpsgd_philox_dump": (C.c_int, [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_int64,
                                      C.c_int64, C.c_void_p, C.c_void_p]),
     "adpsgd_normal_dump": (C.c_int, [C.c_uint64, C.c_uint32, C.c_uint32, C.c_uint32, C.c_int64,
@@ -201,6 +203,17 @@ def adpsgd_average(ctx: int, T: int) -> np.ndarray:
 def adpsgd_step_average(ctx: int, T: int) -> np.ndarray:
     var = np.zeros(T)
     _check(lib.adpsgd_step_average(ctx, var.ctypes.data_as(_DP)))
+    return var
+
+
+def adpsgd_average_noalloc(K: int, P: int, row_stride: int, offsets: Sequence[int], x_ptr: int,
+                           stream: int) -> np.ndarray:
+    """The separate sync of a [K, row_stride] device buffer with no context and no
+    allocation on the device; returns the per-tensor variances."""
+    off = _i64(offsets)
+    var = np.zeros(len(off) - 1)
+    _check(lib.adpsgd_average_noalloc(K, P, row_stride, off.ctypes.data_as(_I64P), len(off) - 1, x_ptr,
+                                      var.ctypes.data_as(_DP), stream))
     return var
 
 

@@ -21,7 +21,7 @@ ROCM_LIB = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "lib")   # roc
 
 DIGEST = LIB + ".digest"   # source digest of the library next to it
 
-HIP_SOURCES = ["kernels.hip"]
+HIP_SOURCES = ["kernels.hip", "noalloc.hip"]
 HOST_SOURCES = ["runtime.cpp", "controller.cpp"]
 
 
