@@ -259,6 +259,30 @@ __device__ __forceinline__ f4 lds_mean(const f4 (*rows)[64], int lane, int W, in
     }
 }
 
+__device__ __forceinline__ f4 shfl_xor4(f4 v, int off) {
+    return f4{__shfl_xor(v.x, off, 64), __shfl_xor(v.y, off, 64), __shfl_xor(v.z, off, 64), __shfl_xor(v.w, off, 64)};
+}
+
+// The replica mean of every group of a tile from the W wave sums in LDS,
+// formed once per group instead of by every wave: wave w takes groups
+// w G .. w G + G - 1 (G = 64 / W), its lane l the wave sum l % W of group
+// w G + l / W, and a butterfly over those W lanes adds them as the pairwise
+// tree does (each pair in the tree's order up to commutation, so the same bits
+// as tree_sum_lds<W>).  The means of the first n groups go to out[64]; callers
+// put a barrier before (the wave sums) and after (the means).  For a block of
+// 16 waves this reads 1/16 of the LDS that every wave reading all 16 sums
+// reads (+2 to +3% for the fused sync at K = 16 and 32; no gain at 8 waves).
+template <int W, int KT>
+__device__ __forceinline__ void group_means(const f4 (*sums)[64], f4 *out, int lane, int w, int n) {
+    static_assert((W & (W - 1)) == 0 && (KT & (KT - 1)) == 0, "power-of-two waves and workers");
+    constexpr int G = 64 / W;
+    const int j = w * G + lane / W, i = lane % W;
+    f4 v = j < n ? sums[i][j] : splat(0.0f);
+#pragma unroll
+    for (int off = 1; off < W; off <<= 1) v = v + shfl_xor4(v, off);
+    if (i == 0) out[j] = v * splat(1.0f / (float)KT);
+}
+
 // Step s.t of a run whose schedule lives on the device: does a sync follow
 // it?  Every thread reads the same state (written only by the reduction
 // kernel after a sync), so the answer is uniform over the launch.
@@ -326,9 +350,12 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     const int W = KT > 0 ? WMAX : (p.s.K + (RD > 0 ? RD : 1) - 1) / (RD > 0 ? RD : 1);
     constexpr bool STEP = MODE != kAverage;
     constexpr bool GN = MODE == kDeviceTrace;
+    // a block of 16 waves forms each group's mean once (group_means)
+    constexpr bool SPLIT = KT > 0 && WMAX >= 16;
     // wave w owns rows R w .. R w + R - 1 and publishes their subtree sum
     __shared__ f4 part[WMAX][64];
     __shared__ f4 mpart[AVGM ? WMAX : 1][64];
+    __shared__ f4 means[SPLIT ? 64 : 1], mmeans[SPLIT && AVGM ? 64 : 1];
     const StepParams &a = p.s;
     bool bcast = true;  // the host-decided modes always average
     if constexpr (MODE == kDevice || MODE == kDeviceTrace) bcast = device_due(p);
@@ -389,9 +416,19 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     }
     if (!measure) return;  // uniform over the block
     __syncthreads();
+    if constexpr (SPLIT) {
+        // groups of the tile with elements in [lo, hi): the lanes that stored a sum
+        const int64_t n64 = (hi - 4 * (lo >> 2) + 3) / 4;
+        const int n = n64 < 64 ? (int)n64 : 64;
+        group_means<WMAX, KT>(part, means, lane, w, n);
+        if (AVGM) group_means<WMAX, KT>(mpart, mmeans, lane, w, n);
+        __syncthreads();
+    }
     double acc = 0.0, gn = 0.0;
     if (active) {
-        const f4 mean = lds_mean<KT, WMAX, RD>(part, lane, W, a.K);
+        f4 mean;
+        if constexpr (SPLIT) mean = means[lane];
+        else mean = lds_mean<KT, WMAX, RD>(part, lane, W, a.K);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             if (!has[r]) continue;
@@ -406,7 +443,9 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             }
         }
         if (avg_m) {
-            const f4 mmean = lds_mean<KT, WMAX, RD>(mpart, lane, W, a.K);
+            f4 mmean;
+            if constexpr (SPLIT) mmean = mmeans[lane];
+            else mmean = lds_mean<KT, WMAX, RD>(mpart, lane, W, a.K);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 if (!has[r]) continue;
