@@ -5,6 +5,7 @@
 #include <cstdlib>
 #include <vector>
 #include <cmath>
+#include <cstring>
 #include "adpsgd.h"
 
 #define CK(x) do { hipError_t e = (x); if (e != hipSuccess) { printf("HIP error %s at %d\n", hipGetErrorString(e), __LINE__); return 1;} } while(0)
@@ -76,7 +77,88 @@ static int one(int K, std::vector<int64_t> sizes, int mode, int p_init, int64_t 
     return 0;
 }
 
+// A constant-period run replayed as a HIP graph (timing off, hybrid policy) on
+// the null stream or a stream of the caller's: captured once, replayed, captured
+// again for a new start state and after a launch-shape change; each replay must
+// leave the bits of the host-waiting policy's eager launches.  Then the
+// no-allocation sync on copies of the replicas against adpsgd_average.
+static int graph_and_noalloc(bool own_stream) {
+    const std::vector<int64_t> sizes = {5000, 77, 1, 0, 1024, 3, 70000, 263};
+    std::vector<int64_t> off(1, 0);
+    for (auto v : sizes) off.push_back(off.back() + v);
+    const int T = (int)sizes.size(), K = 4;
+    const int64_t P = off.back(), N = 60;
+    adpsgd_hparams hp = hp_of(ADPSGD_PERIOD_CONST, 4, N, 0);
+    hipStream_t st = nullptr;
+    if (own_stream) CK(hipStreamCreateWithFlags(&st, hipStreamNonBlocking));
+    std::vector<float> ref((size_t)K * P), got((size_t)K * P);
+    for (int pass = 0; pass < 2; ++pass) {   // pass 0: eager reference; pass 1: graph replays
+        size_t ws = adpsgd_workspace_bytes(K, P, T, off.data());
+        float *x, *m, *h, *xs; void *w;
+        CK(hipMalloc(&x, 4 * (size_t)K * P)); CK(hipMalloc(&m, 4 * (size_t)K * P));
+        CK(hipMalloc(&h, 4 * (size_t)P)); CK(hipMalloc(&xs, 4 * (size_t)P)); CK(hipMalloc(&w, ws));
+        adpsgd_buffers b{x, m, h, xs, w, ws, st, 0};
+        adpsgd_ctx *c = nullptr;
+        OKC(adpsgd_init(K, P, off.data(), T, &hp, &b, &c));
+        OKC(adpsgd_set_launch_policy(c, pass == 0 ? ADPSGD_LAUNCH_HOST : ADPSGD_LAUNCH_HYBRID));
+        std::vector<adpsgd_sync_rec> log(N);
+        std::vector<double> var((size_t)N * T);
+        int64_t n = 0;
+        for (int rep = 0; rep < 3; ++rep) {
+            OKC(adpsgd_reset(c));
+            OKC(adpsgd_run(c, N, log.data(), rep == 1 ? 2 : (int64_t)log.size(), rep == 2 ? nullptr : var.data(), &n));
+            CK(hipMemcpy(pass == 0 ? ref.data() : got.data(), x, 4 * (size_t)K * P, hipMemcpyDeviceToHost));
+            if (pass == 1 && std::memcmp(ref.data(), got.data(), 4 * (size_t)K * P) != 0) {
+                printf("graph replay %d differs from the eager run\n", rep); return 1;
+            }
+            std::vector<double> v(T);
+            OKC(adpsgd_local_steps(c, 2));   // eager work between the replays
+            OKC(adpsgd_average(c, v.data()));
+        }
+        OKC(adpsgd_run(c, 7, log.data(), (int64_t)log.size(), var.data(), &n));   // a new start state
+        OKC(adpsgd_set_step_launch(c, 128, 0, 1));
+        OKC(adpsgd_reset(c));
+        OKC(adpsgd_run(c, N, log.data(), (int64_t)log.size(), var.data(), &n));   // a new launch shape
+        adpsgd_timing tm;
+        OKC(adpsgd_get_timing(c, &tm));
+        if (pass == 1 && (tm.graph_captures != 3 || tm.graph_replays != 5)) {
+            printf("graph captures %lld replays %lld\n", (long long)tm.graph_captures, (long long)tm.graph_replays);
+            return 1;
+        }
+        if (pass == 1) {
+            // the no-allocation sync on a copy of the replicas, against adpsgd_average
+            float *x2;
+            CK(hipMalloc(&x2, 4 * (size_t)K * P));
+            OKC(adpsgd_local_steps(c, 3));
+            // the steps are asynchronous on the context's stream, and a device-to-device
+            // copy does not block the host: copy on that stream and wait for it
+            CK(hipMemcpyAsync(x2, x, 4 * (size_t)K * P, hipMemcpyDeviceToDevice, st));
+            CK(hipStreamSynchronize(st));
+            std::vector<double> v1(T), v2(T);
+            OKC(adpsgd_average(c, v1.data()));
+            OKC(adpsgd_average_noalloc(K, P, 0, off.data(), T, x2, v2.data(), st));
+            std::vector<float> a((size_t)K * P), bb((size_t)K * P);
+            CK(hipMemcpy(a.data(), x, 4 * (size_t)K * P, hipMemcpyDeviceToHost));
+            CK(hipMemcpy(bb.data(), x2, 4 * (size_t)K * P, hipMemcpyDeviceToHost));
+            if (std::memcmp(a.data(), bb.data(), 4 * (size_t)K * P) != 0) { printf("no-alloc sync differs\n"); return 1; }
+            for (int i = 0; i < T; ++i)
+                if (std::fabs(v1[i] - v2[i]) > 1e-12 * std::fabs(v1[i])) { printf("no-alloc variance differs\n"); return 1; }
+            // a smaller problem next (K = 2, the first three tensors)
+            const int64_t P2 = off[3];
+            OKC(adpsgd_average_noalloc(2, P2, P, off.data(), 3, x2, v2.data(), st));
+            CK(hipFree(x2));
+        }
+        OKC(adpsgd_destroy(c));
+        CK(hipFree(x)); CK(hipFree(m)); CK(hipFree(h)); CK(hipFree(xs)); CK(hipFree(w));
+    }
+    if (st) CK(hipStreamDestroy(st));
+    printf("ok graph replays and no-alloc sync (%s stream)\n", own_stream ? "own" : "null");
+    fflush(stdout);
+    return 0;
+}
+
 int main() {
+    if (graph_and_noalloc(false) || graph_and_noalloc(true)) return 1;
     const std::vector<int64_t> ragged = {5000, 77, 1, 0, 1024, 3, 70000, 263};
     // more chunk partials than the finishing block's LDS holds: the window
     // tables (a split run of small tensors and one tensor of over 32 chunks)

@@ -16,8 +16,9 @@ INC="-I$ROOT/include -I$SRC"
 FL="-O1 -g -std=c++17 -fno-omit-frame-pointer -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined"
 HIPCC=${HIPCC:-/opt/rocm/bin/hipcc}
 $HIPCC $FL $INC --offload-arch=gfx950 -ffp-contract=off -Xclang -target-feature -Xclang -packed-fp32-ops -x hip -c "$SRC/kernels.hip" -o "$OUT/kernels.o"
+$HIPCC $FL $INC --offload-arch=gfx950 -ffp-contract=off -Xclang -target-feature -Xclang -packed-fp32-ops -x hip -c "$SRC/noalloc.hip" -o "$OUT/noalloc.o"
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -ffp-contract=off -c "$SRC/runtime.cpp" -o "$OUT/runtime.o"
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -ffp-contract=off -c "$SRC/controller.cpp" -o "$OUT/controller.o"
 $HIPCC $FL $INC -D__HIP_PLATFORM_AMD__ -c "$HERE/abi_asan_driver.cpp" -o "$OUT/driver.o"
-$HIPCC -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined --offload-arch=gfx950 "$OUT"/kernels.o "$OUT"/runtime.o "$OUT"/controller.o "$OUT"/driver.o -L/opt/rocm/lib -lrocprofiler-sdk-roctx -Wl,-rpath,/opt/rocm/lib -o "$OUT/abi_asan_driver"
+$HIPCC -Xarch_host -fsanitize=address -Xarch_host -fsanitize=undefined --offload-arch=gfx950 "$OUT"/kernels.o "$OUT"/noalloc.o "$OUT"/runtime.o "$OUT"/controller.o "$OUT"/driver.o -L/opt/rocm/lib -lrocprofiler-sdk-roctx -Wl,-rpath,/opt/rocm/lib -o "$OUT/abi_asan_driver"
 echo "$OUT/abi_asan_driver"
