@@ -362,13 +362,15 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
     const bool measure = MODE != kDevice || bcast;
     const bool avg_m = AVGM && bcast;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int64_t ti = p.s.block0 + blockIdx.x;
-    const Tile tile = p.tiles[ti];
-    const int64_t lo = tile.start, hi = tile.start + tile.len;
+    // the block's aligned chunk and its tiles (one per tensor in it)
+    const int64_t c = p.s.block0 + blockIdx.x;
+    const int64_t lo = c * kTileElems, hi = lo + kTileElems < a.P ? lo + kTileElems : a.P;
+    const int32_t s0 = p.chunk_seg[c], s1 = p.chunk_seg[c + 1];
+    const bool one_tile = s1 - s0 == 1;   // uniform over the block
     const int64_t g = (lo >> 2) + lane;
     const int64_t e0 = 4 * g;
     const bool active = e0 < hi;
-    const bool full = VEC && e0 >= lo && e0 + 4 <= hi;
+    const bool full = VEC && e0 + 4 <= hi;
     // row R w + r exists (only the last wave's second row can be missing)
     bool has[R];
 #pragma unroll
@@ -424,7 +426,10 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
         if (AVGM) group_means<WMAX, KT>(mpart, mmeans, lane, w, n);
         __syncthreads();
     }
+    // a chunk of one tile sums its squared deviations per row; a chunk of
+    // several keeps them per element (over the rows), to split them by tile
     double acc = 0.0, gn = 0.0;
+    double acc4[4] = {0.0, 0.0, 0.0, 0.0}, gn4[4] = {0.0, 0.0, 0.0, 0.0};
     if (active) {
         f4 mean;
         if constexpr (SPLIT) mean = means[lane];
@@ -436,7 +441,14 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
             const f4 dk = mean - xr[r];
             f4 d2 = dk * dk;
             if (!full) d2 = mask4(d2, e0, lo, hi);
-            acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
+            if (one_tile) {
+                acc += ((double)d2.x + (double)d2.y) + ((double)d2.z + (double)d2.w);
+            } else {
+                acc4[0] += (double)d2.x;
+                acc4[1] += (double)d2.y;
+                acc4[2] += (double)d2.z;
+                acc4[3] += (double)d2.w;
+            }
             if (bcast) {
                 float *xrow = a.x + (int64_t)(R * w + r) * a.ld + e0;
                 if (full) st4<NT>(xrow, mean); else st4_masked(xrow, mean, e0, lo, hi);
@@ -453,14 +465,49 @@ __global__ void __launch_bounds__((64 * sync_waves<KT, MODE>())) k_sync_lds(Sync
                 if (full) st4<NT>(mrow, mmean); else st4_masked(mrow, mmean, e0, lo, hi);
             }
         }
-        if (GN && w == 0) gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
+        if (GN && w == 0) {
+            if (one_tile) {
+                gn = grad_norm2(a, mean, h, xs, full, e0, lo, hi);
+            } else {
+                const f4 gr = fma4(h, mean - xs, splat(a.wd) * mean);
+                f4 g2 = gr * gr;
+                if (!full) g2 = mask4(g2, e0, lo, hi);
+                gn4[0] = g2.x;
+                gn4[1] = g2.y;
+                gn4[2] = g2.z;
+                gn4[3] = g2.w;
+            }
+        }
     }
-    Pair total;
-    if constexpr (KT > 0) total = block_sum2<WMAX, GN>(acc, gn);
-    else total = block_sum2_waves<GN>(acc, gn, W);
-    if (threadIdx.x == 0) {
-        p.partials[2 * ti] = total.a;
-        p.partials[2 * ti + 1] = total.b;
+    if (one_tile) {
+        Pair total;
+        if constexpr (KT > 0) total = block_sum2<WMAX, GN>(acc, gn);
+        else total = block_sum2_waves<GN>(acc, gn, W);
+        if (threadIdx.x == 0) {
+            p.partials[2 * s0] = total.a;
+            p.partials[2 * s0 + 1] = total.b;
+        }
+        return;
+    }
+    // several tiles (tensors) in the chunk: one fixed-order block sum each, of
+    // the elements in its range
+    for (int32_t sgi = s0; sgi < s1; ++sgi) {
+        const Tile t = p.tiles[sgi];
+        double v = 0.0, gv = 0.0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (in(e0 + j, t.start, t.start + t.len)) {
+                v += acc4[j];
+                gv += gn4[j];
+            }
+        Pair total;
+        if constexpr (KT > 0) total = block_sum2<WMAX, GN>(v, gv);
+        else total = block_sum2_waves<GN>(v, gv, W);
+        if (threadIdx.x == 0) {
+            p.partials[2 * sgi] = total.a;
+            p.partials[2 * sgi + 1] = total.b;
+        }
+        __syncthreads();   // the block sum's LDS is used again for the next tile
     }
 }
 
@@ -895,14 +942,14 @@ constexpr int any_k_rows(int K) { return K == 3 ? 1 : (K <= 32 ? 2 : 4); }
 constexpr int any_k_waves(int K) { return (K + any_k_rows(K) - 1) / any_k_rows(K); }
 
 template <int KT, bool VEC, bool NT, int MODE, bool AVGM, int RD, bool RAGGED>
-hipError_t sync_variant(const SyncParams &p, int64_t n_tiles, int cap, hipStream_t st) {
+hipError_t sync_variant(const SyncParams &p, int64_t, int cap, hipStream_t st) {
     const int threads = KT > 0 ? 64 * sync_waves<KT, MODE>() : 64 * any_k_waves(p.s.K);
     int lds = 0;
     if (cap > 0) {   // (the attribute query only when it is needed: not under graph capture)
         static const size_t own = static_lds_of(k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED>);
         lds = cap_lds(cap, own);
     }
-    return in_pieces(n_tiles, threads, [&](int64_t b0, unsigned nb) {
+    return in_pieces(p.n_chunks, threads, [&](int64_t b0, unsigned nb) {   // a block per chunk
         SyncParams q = p;
         q.s.block0 = b0;
         k_sync_lds<KT, VEC, NT, MODE, AVGM, RD, RAGGED><<<dim3(nb), dim3(threads), lds, st>>>(q);
@@ -1026,6 +1073,21 @@ hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool
                                   : sync_dispatch<0, 4, true>(p, n_tiles, mode, avg_m, vec, nt, cap, st);
         }
     }
+}
+
+bool chunk_segments(const std::vector<Tile> &tiles, int64_t n_chunks, std::vector<int32_t> *out) {
+    out->assign((size_t)n_chunks + 1, -1);
+    int64_t prev = -1;
+    for (size_t sgi = 0; sgi < tiles.size(); ++sgi) {
+        const int64_t c = tiles[sgi].start / kTileElems;
+        if (c < 0 || c >= n_chunks || c < prev) return false;
+        if (c != prev) (*out)[(size_t)c] = (int32_t)sgi;
+        prev = c;
+    }
+    (*out)[(size_t)n_chunks] = (int32_t)tiles.size();
+    for (int64_t c = 0; c < n_chunks; ++c)
+        if ((*out)[(size_t)c] < 0) return false;
+    return true;
 }
 
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st) {

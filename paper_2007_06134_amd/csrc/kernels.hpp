@@ -69,6 +69,13 @@ struct SyncParams {
     StepParams s;      // x, m, P, K; the step fields are used by the modes with a step
     const Tile *tiles;
     double *partials;  // [2 n_tiles]: per tile, sum of sum_k (xbar - x_k)^2, gradient norm^2
+    // The sync-tile kernel (not the loop kernel) takes one block per aligned
+    // chunk of kTileElems elements, [c kTileElems, (c + 1) kTileElems) cut at P,
+    // whatever tensors it holds: its tiles are chunk_seg[c] .. chunk_seg[c+1]-1
+    // (every chunk holds at least one), so a tensor boundary inside a chunk
+    // costs no block of its own.
+    const int32_t *chunk_seg;  // [n_chunks + 1]
+    int64_t n_chunks;          // ceil(P / kTileElems)
     // modes decided on the device: step s.t syncs iff Algorithm 2's counter,
     // read from *sched at block start, says so (the state is written only by
     // the reduction kernel that follows a sync)
@@ -120,6 +127,9 @@ enum SyncMode : int { kAverage = 0, kFused = 1, kDevice = 2, kDeviceTrace = 3 };
 // The loop kernel (K above 64, the separate sync at K = 3) ignores it.
 hipError_t launch_tile_sync(const SyncParams &p, int64_t n_tiles, int mode, bool avg_m, bool vec,
                             bool nontemporal, int cap, hipStream_t st);
+// chunk_seg (SyncParams) of a tile table: out[c] = the first tile that starts in
+// chunk c, out[n_chunks] = n_tiles; false if some chunk holds no tile.
+bool chunk_segments(const std::vector<Tile> &tiles, int64_t n_chunks, std::vector<int32_t> *out);
 // Waves per block of the sync-tile kernel for K workers in a mode (0 when K
 // takes the loop kernel).
 int sync_tile_waves(int K, int mode);

@@ -1,5 +1,7 @@
 // adpsgd_average_noalloc: the separate synchronization (Algorithm 2, lines
 // 10-12) for callers that cannot allocate device memory, with no context.
+// Its scratch also holds the first tile of every aligned chunk, the block
+// index of the sync-tile kernel.
 //
 // It runs the same sync-tile kernel as adpsgd_average (so the replicas get the
 // same bits), but every buffer the kernels need beyond the caller's x lives in
@@ -59,16 +61,17 @@ __host__ __device__ inline int64_t tile_count(int64_t a, int64_t b) {
 
 // Byte offsets of the scratch regions for T tensors and n_tiles tiles.
 struct ScratchLayout {
-    size_t offsets, first_tile, tiles, partials, var, total;
+    size_t offsets, first_tile, tiles, partials, var, chunk_seg, total;
 };
-ScratchLayout scratch_layout(int32_t T, int64_t n_tiles) {
+ScratchLayout scratch_layout(int32_t T, int64_t n_tiles, int64_t n_chunks) {
     ScratchLayout l;
     l.offsets = 0;
     l.first_tile = align256(l.offsets + sizeof(int64_t) * ((size_t)T + 1));
     l.tiles = align256(l.first_tile + sizeof(int64_t) * ((size_t)T + 1));
     l.partials = align256(l.tiles + sizeof(Tile) * (size_t)n_tiles);
     l.var = align256(l.partials + 2 * sizeof(double) * (size_t)n_tiles);
-    l.total = align256(l.var + sizeof(double) * (size_t)T);
+    l.chunk_seg = align256(l.var + sizeof(double) * (size_t)T);
+    l.total = align256(l.chunk_seg + sizeof(int32_t) * ((size_t)n_chunks + 1));
     return l;
 }
 
@@ -120,6 +123,17 @@ __global__ void __launch_bounds__(kThreads) k_build_tiles(const int64_t *off, co
     tiles[i] = Tile{start, (int32_t)((cut < b ? cut : b) - start), lo};
 }
 
+// The first tile of every aligned chunk (the sync-tile kernel's blocks), one
+// thread per tile: a tile that starts a chunk's run of tiles records itself.
+__global__ void __launch_bounds__(kThreads) k_chunk_tiles(const Tile *tiles, int64_t n_tiles, int64_t n_chunks,
+                                                          int32_t *chunk_seg) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i == 0) chunk_seg[n_chunks] = (int32_t)n_tiles;
+    if (i >= n_tiles) return;
+    const int64_t c = tiles[i].start / kTileElems;
+    if (i == 0 || tiles[i - 1].start / kTileElems != c) chunk_seg[c] = (int32_t)i;
+}
+
 // One block per tensor: the sum of its tile partials (strided over the
 // threads, then a fixed-order block sum), divided by K.  Empty tensors get 0.
 __global__ void __launch_bounds__(kThreads) k_tensor_var(const int64_t *first_tile, const double *partials,
@@ -160,7 +174,8 @@ extern "C" int adpsgd_average_noalloc(int32_t K, int64_t P, int64_t row_stride, 
     if (row_stride < 0 || (row_stride > 0 && row_stride < P)) return fail(ADPSGD_EINVAL, "row_stride must be 0 or >= P");
     if (P > 0 && (!x || reinterpret_cast<uintptr_t>(x) % 16 != 0))
         return fail(ADPSGD_EINVAL, "x must be non-NULL and 16-byte aligned");
-    const ScratchLayout lay = scratch_layout(T, n_tiles);
+    const int64_t n_chunks = (P + kTileElems - 1) / kTileElems;
+    const ScratchLayout lay = scratch_layout(T, n_tiles, n_chunks);
     if (lay.total > kScratchBytes)
         return fail(ADPSGD_EINVAL, "problem needs " + std::to_string(lay.total) + " bytes of scratch; the limit is " +
                                        std::to_string(kScratchBytes) + " (about 2 million sync tiles)");
@@ -170,6 +185,7 @@ extern "C" int adpsgd_average_noalloc(int32_t K, int64_t P, int64_t row_stride, 
     int64_t *d_off = reinterpret_cast<int64_t *>(base + lay.offsets);
     int64_t *d_first = reinterpret_cast<int64_t *>(base + lay.first_tile);
     Tile *d_tiles = reinterpret_cast<Tile *>(base + lay.tiles);
+    int32_t *d_chunk_seg = reinterpret_cast<int32_t *>(base + lay.chunk_seg);
     double *d_part = reinterpret_cast<double *>(base + lay.partials);
     double *d_var = reinterpret_cast<double *>(base + lay.var);
 
@@ -184,6 +200,9 @@ extern "C" int adpsgd_average_noalloc(int32_t K, int64_t P, int64_t row_stride, 
         k_build_tiles<<<(unsigned)((n_tiles + kThreads - 1) / kThreads), kThreads, 0, st>>>(d_off, d_first, T, n_tiles,
                                                                                             d_tiles);
         if ((e = hipGetLastError()) != hipSuccess) return hip_err(e, "tile table launch");
+        k_chunk_tiles<<<(unsigned)((n_tiles + kThreads - 1) / kThreads), kThreads, 0, st>>>(d_tiles, n_tiles, n_chunks,
+                                                                                            d_chunk_seg);
+        if ((e = hipGetLastError()) != hipSuccess) return hip_err(e, "chunk table launch");
         SyncParams sp{};
         sp.s.x = x;
         sp.s.ld = ld;
@@ -192,6 +211,8 @@ extern "C" int adpsgd_average_noalloc(int32_t K, int64_t P, int64_t row_stride, 
         sp.s.K = K;
         sp.tiles = d_tiles;
         sp.partials = d_part;
+        sp.chunk_seg = d_chunk_seg;
+        sp.n_chunks = n_chunks;
         const bool vec = ld % 4 == 0;
         const bool nt = (double)K * (double)P * 8.0 > 256.0 * 1024 * 1024;   // beyond the last-level cache
         if ((e = launch_tile_sync(sp, n_tiles, kAverage, false, vec, nt, 0, st)) != hipSuccess)

@@ -118,6 +118,7 @@ int64_t tiles_of(int64_t a, int64_t b) { return b > a ? (b + kTileElems - 1) / k
 
 struct Plan {
     int64_t n_tiles = 0, n_chunks = 0;
+    int64_t n_aligned = 0;  // aligned chunks of kTileElems elements (a sync-tile block each)
     int32_t chunk_tiles = kChunkTiles;
     int32_t n_windows = 0;  // windows of tensors for k_reduce_windows (0: none)
 };
@@ -125,6 +126,7 @@ struct Plan {
 Plan count_plan(int32_t T, const int64_t *off) {
     Plan pl;
     for (int32_t tau = 0; tau < T; ++tau) pl.n_tiles += tiles_of(off[tau], off[tau + 1]);
+    pl.n_aligned = (off[T] + kTileElems - 1) / kTileElems;
     pl.chunk_tiles = pl.n_tiles <= kDirectMaxTiles ? 1 : kChunkTiles;
     std::vector<int32_t> chunk_begin(T + 1, 0);
     for (int32_t tau = 0; tau < T; ++tau) {
@@ -159,7 +161,7 @@ void build_plan(int32_t T, const int64_t *off, int32_t chunk_tiles, std::vector<
 
 struct Layout {
     size_t tiles, chunks, chunk_begin, large, tile_partials, chunk_partials, acc, win_begin, win_partials, sched,
-        total;
+        chunk_seg, total;
 };
 
 // A record slot (pinned host memory the reduction writes directly): the
@@ -179,7 +181,8 @@ Layout layout_for(const Plan &pl, int32_t T) {
     l.win_begin = align_up(l.acc + 2 * sizeof(double) * (size_t)T, 256);
     l.win_partials = align_up(l.win_begin + sizeof(int32_t) * (size_t)(pl.n_windows + 1), 256);
     l.sched = align_up(l.win_partials + 2 * sizeof(double) * at_least_one(pl.n_windows), 256);
-    l.total = align_up(l.sched + sizeof(SchedState), 256);
+    l.chunk_seg = align_up(l.sched + sizeof(SchedState), 256);
+    l.total = align_up(l.chunk_seg + sizeof(int32_t) * (size_t)(pl.n_aligned + 1), 256);
     return l;
 }
 
@@ -226,6 +229,8 @@ struct adpsgd_ctx {
     Chunk *d_chunks = nullptr;
     int32_t *d_chunk_begin = nullptr;
     int32_t *d_large = nullptr;
+    std::vector<int32_t> chunk_seg; // first tile of each aligned chunk (the sync-tile kernel's blocks)
+    int32_t *d_chunk_seg = nullptr;
     bool chunks_are_tiles = false;  // every tile is its own chunk (small problems)
     double *d_tile_partials = nullptr;
     double *d_chunk_partials = nullptr;
@@ -402,6 +407,8 @@ SyncParams sync_params(const adpsgd_ctx *c, int64_t t) {
     sp.s = step_params(c, t);
     sp.tiles = c->d_tiles;
     sp.partials = c->d_tile_partials;
+    sp.chunk_seg = c->d_chunk_seg;
+    sp.n_chunks = (int64_t)c->chunk_seg.size() - 1;
     sp.sched = c->d_sched;
     sp.rule = rule_of(&c->hp);
     return sp;
@@ -696,6 +703,11 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->d_chunk_partials = (double *)(ws + lay.chunk_partials);
     c->d_acc = (double *)(ws + lay.acc);
     c->d_sched = (SchedState *)(ws + lay.sched);
+    c->d_chunk_seg = (int32_t *)(ws + lay.chunk_seg);
+    if (!chunk_segments(c->tiles, plan.n_aligned, &c->chunk_seg)) {
+        release(c);
+        return fail(ADPSGD_EINVAL, "internal: the tile table does not cover every aligned chunk");
+    }
     c->slot_bytes = slot_bytes_for(T);
 
     auto bail = [&](hipError_t e, const char *what) {
@@ -728,6 +740,9 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     if ((e = hipMemcpyAsync(c->d_chunk_begin, c->chunk_begin.data(), sizeof(int32_t) * (T + 1),
                             hipMemcpyHostToDevice, c->stream)) != hipSuccess)
         return bail(e, "copy chunk offsets");
+    if ((e = hipMemcpyAsync(c->d_chunk_seg, c->chunk_seg.data(), sizeof(int32_t) * c->chunk_seg.size(),
+                            hipMemcpyHostToDevice, c->stream)) != hipSuccess)
+        return bail(e, "copy the aligned chunks' tiles");
     if (!c->large.empty() &&
         (e = hipMemcpyAsync(c->d_large, c->large.data(), sizeof(int32_t) * c->large.size(), hipMemcpyHostToDevice,
                             c->stream)) != hipSuccess)
