@@ -141,10 +141,23 @@ typedef struct {
                                so whole float4 groups move with vector accesses when P is
                                not a multiple of 4 (about 2x faster than P rows packed back
                                to back); a multiple of 256 also starts every row on a 1 KB
-                               boundary, so a wave's 1 KB of a row is one aligned kilobyte
-                               (3% faster at P = 138M than rows half a kilobyte apart).
+                               boundary, so a wave's 1 KB of a row is one aligned kilobyte.
+                               adpsgd_padded_row_stride gives the stride to use with the
+                               single-allocation layout described there.
                                The library never touches the padding.                       */
 } adpsgd_buffers;
+
+/* The row stride (in floats) for P parameters that the fastest buffer layout
+ * uses: the least 256 n >= P with n odd (0 for P <= 0).  The layout is one
+ * allocation of 2K + 2 rows of that stride holding the K rows of x, then the
+ * K rows of m, then h and xstar as rows 2K and 2K + 1.  Every kernel streams
+ * all of those rows at the same element offset at once, and how far apart
+ * they start decides how fast (through how HBM addresses interleave over
+ * channels, presumably): measured on MI355X at K = 8, P = 138M, this layout
+ * runs the local step 1% and the fused step + sync 2.5% faster than x, m, h
+ * and xstar in separate allocations, and the fused step + sync up to 10%
+ * faster than rows an even number of kilobytes apart. */
+ADPSGD_API int64_t adpsgd_padded_row_stride(int64_t P);
 
 /* Controller state on the host (Algorithm 2, lines 1-3).  x and m are the
  * device part of the state and stay in the caller's buffers. */

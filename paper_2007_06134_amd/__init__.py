@@ -19,8 +19,8 @@ from ._native import (  # noqa: F401
     adpsgd_run_traced, adpsgd_step_rec,
     adpsgd_sched_init, adpsgd_sched_on_sync, adpsgd_sched_step, adpsgd_schedule, adpsgd_set_launch_policy, adpsgd_set_state, adpsgd_set_timing,
     adpsgd_get_step_launch, adpsgd_set_step_launch,
-    adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing, adpsgd_workspace_bytes,
-    make_hparams,
+    adpsgd_padded_row_stride, adpsgd_state, adpsgd_step_average, adpsgd_sync_rec, adpsgd_timing,
+    adpsgd_workspace_bytes, make_hparams,
 )
 
 
@@ -40,12 +40,15 @@ class Adpsgd:
 
     x, m: float32 [K, P]; h, xstar: float32 [P]; workspace: uint8 sized by
     adpsgd_workspace_bytes.  The stream is the torch stream current at
-    construction (or the one passed in).  With pad_rows (default) and P not a
-    multiple of 256, x and m are views of [K, P rounded up to 256] buffers, so
-    that every row starts on a 1 KB boundary: the kernels then move whole
-    float4 groups, and each 64-lane wave's 1 KB of a row is one aligned
-    kilobyte (at P = 138M, where rows would start half a kilobyte apart, the
-    local step runs 3% faster).  pad_rows=False packs the rows back to back.
+    construction (or the one passed in).  With pad_rows (default), x, m, h and
+    xstar are views of the rows of ONE [2K + 2, row_stride] buffer (x rows,
+    then m rows, then h, then xstar), row_stride = adpsgd_padded_row_stride(P):
+    256 n floats with n odd.  Every row then starts on a 1 KB boundary (the
+    kernels move whole float4 groups, and each 64-lane wave's 1 KB of a row is
+    one aligned kilobyte), and the rows that a kernel streams together start an
+    odd number of kilobytes apart, which measures fastest on MI355X.
+    pad_rows=False allocates x and m as packed [K, P] buffers and h and xstar
+    on their own.
     """
 
     def __init__(self, K: int, offsets, hp: adpsgd_hparams, device="cuda", stream=None, pad_rows: bool = True):
@@ -63,13 +66,20 @@ class Adpsgd:
         if nbytes == 0:
             raise ValueError("invalid K, P or tensor offsets")
         alloc = dict(device=self.device, dtype=torch.float32)
-        self.row_stride = (self.P + 255) // 256 * 256 if pad_rows else self.P
-        self._x_rows = torch.empty((self.K, self.row_stride), **alloc)
-        self._m_rows = torch.empty((self.K, self.row_stride), **alloc)
+        K = self.K
+        if pad_rows:
+            self.row_stride = adpsgd_padded_row_stride(self.P)
+            self._rows = torch.empty((2 * K + 2, self.row_stride), **alloc)
+            self._x_rows, self._m_rows = self._rows[:K], self._rows[K:2 * K]
+            self.h, self.xstar = self._rows[2 * K, :self.P], self._rows[2 * K + 1, :self.P]
+        else:
+            self.row_stride = self.P
+            self._x_rows = torch.empty((K, self.P), **alloc)
+            self._m_rows = torch.empty((K, self.P), **alloc)
+            self.h = torch.empty((self.P,), **alloc)
+            self.xstar = torch.empty((self.P,), **alloc)
         self.x = self._x_rows[:, :self.P]
         self.m = self._m_rows[:, :self.P]
-        self.h = torch.empty((self.P,), **alloc)
-        self.xstar = torch.empty((self.P,), **alloc)
         self.workspace = torch.empty((nbytes,), device=self.device, dtype=torch.uint8)
         self.buf = adpsgd_buffers(x=self._x_rows.data_ptr(), m=self._m_rows.data_ptr(), h=self.h.data_ptr(),
                                   xstar=self.xstar.data_ptr(), workspace=self.workspace.data_ptr(),

@@ -109,6 +109,7 @@ _DP = C.POINTER(C.c_double)
 
 _SIGS = {
     "adpsgd_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int64, C.c_int32, _I64P]),
+    "adpsgd_padded_row_stride": (C.c_int64, [C.c_int64]),
     "adpsgd_init": (C.c_int, [C.c_int32, C.c_int64, _I64P, C.c_int32, C.POINTER(adpsgd_hparams),
                               C.POINTER(adpsgd_buffers), C.POINTER(_CTX)]),
     "adpsgd_reset": (C.c_int, [_CTX]),
@@ -176,6 +177,10 @@ def make_hparams(seed, sigma, momentum, weight_decay, h_lo, h_hi, lr_kind, lr0, 
 def adpsgd_workspace_bytes(K: int, P: int, offsets: Sequence[int]) -> int:
     off = _i64(offsets)
     return int(lib.adpsgd_workspace_bytes(K, P, len(off) - 1, off.ctypes.data_as(_I64P)))
+
+
+def adpsgd_padded_row_stride(P: int) -> int:
+    return int(lib.adpsgd_padded_row_stride(P))
 
 
 def adpsgd_init(K: int, P: int, offsets: Sequence[int], hp: adpsgd_hparams, buf: adpsgd_buffers) -> int:

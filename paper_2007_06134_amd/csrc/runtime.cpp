@@ -641,6 +641,12 @@ hipError_t tune_average_cap(adpsgd_ctx *c) {
 
 extern "C" const char *adpsgd_last_error(void) { return g_last_error.c_str(); }
 
+extern "C" int64_t adpsgd_padded_row_stride(int64_t P) {
+    if (P <= 0) return 0;
+    const int64_t n = (P - 1) / 256 + 1;
+    return 256 * (n | 1);
+}
+
 extern "C" size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const int64_t *offsets) {
     std::string why;
     if (!shape_valid(K, P, T, offsets, &why)) return 0;

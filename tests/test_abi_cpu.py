@@ -281,6 +281,20 @@ def test_workspace_bytes_grows_with_tiles(A):
     assert A.adpsgd_workspace_bytes(65536, 8, [0, 8]) > 0  # the largest worker count
 
 
+@pytest.mark.parametrize("P,stride", [
+    (0, 0), (-5, 0), (1, 256), (256, 256), (257, 768), (512, 768), (768, 768), (769, 1280),
+    (138_000_000, 138_000_128),      # 539063 kilobytes: odd already
+    (25_600_000, 25_600_256),        # 100000 kilobytes: one more
+])
+def test_padded_row_stride(A, P, stride):
+    # the least 256 n >= P with n odd: rows of the one-buffer layout start an
+    # odd number of kilobytes apart
+    s = A.adpsgd_padded_row_stride(P)
+    assert s == stride
+    if P > 0:
+        assert s >= P and s % 256 == 0 and (s // 256) % 2 == 1
+
+
 def test_null_context_and_dump_ranges(A):
     assert A._native.lib.adpsgd_local_steps(None, 1) == A.EINVAL
     assert A._native.lib.adpsgd_destroy(None) == A.OK
