@@ -244,6 +244,10 @@ struct adpsgd_ctx {
     adpsgd_state st{};
     bool vec = true;                // row stride % 4 == 0: rows 16-byte aligned, dwordx4 groups
     bool nontemporal = false;       // stream x and m past the caches (large working sets)
+    // the sync-tile kernel's choice of the same, timed at init on large working
+    // sets: the step + sync modes (fused, device-decided, traced) and the separate sync
+    bool sync_nt = false;
+    bool average_nt = false;
     int32_t policy = ADPSGD_LAUNCH_HYBRID;
     StepShape step_shape{256, 0, 1};   // launch shape of the plain local step in use
     StepShape tuned_shape{256, 0, 1};  // the fastest one measured at init
@@ -459,7 +463,8 @@ int enqueue_sync(adpsgd_ctx *c, int mode, int64_t t, int slot, bool ctl, int64_t
     int rc = timed_launch(
         c, kind,
         [&] {
-            return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
+            return launch_tile_sync(sp, n_tiles, mode, c->hp.avg_momentum != 0, c->vec,
+                                    mode == kAverage ? c->average_nt : c->sync_nt,
                                     mode == kAverage ? c->average_cap : 0, c->stream);
         },
         step_seq);
@@ -498,8 +503,8 @@ int capture_run(adpsgd_ctx *c, int64_t t0, const std::vector<char> &due, int64_t
         if (!due[i]) {
             e = launch_local_step(step_params(c, t), c->vec, c->nontemporal, c->step_shape, cs);
         } else {
-            e = launch_tile_sync(sync_params(c, t), n_tiles, kFused, c->hp.avg_momentum != 0, c->vec, c->nontemporal,
-                                 0, cs);
+            e = launch_tile_sync(sync_params(c, t), n_tiles, kFused, c->hp.avg_momentum != 0, c->vec, c->sync_nt, 0,
+                                 cs);
             if (e == hipSuccess)
                 e = launch_reduce(reduce_params(c, kFused, t, c->d_gslots + (size_t)j * c->slot_bytes, true), cs);
             ++j;
@@ -616,24 +621,97 @@ hipError_t tune_step_shape(adpsgd_ctx *c) {
     return e;
 }
 
+// The fastest of n launch sequences, each timed in a block of its own: one
+// untimed call (which also pays for what the sequence before it left in the
+// caches), then `reps` timed calls back to back; two passes over the
+// variants, the smaller mean of the two counts.
+template <class Launch>
+hipError_t fastest_in_blocks(adpsgd_ctx *c, int n, int reps, Launch launch, int *win) {
+    if (n < 1 || n > kMaxVariants || reps < 1) return hipErrorInvalidValue;
+    hipEvent_t ev[2] = {};
+    hipError_t e = hipEventCreate(&ev[0]);
+    if (e == hipSuccess) e = hipEventCreate(&ev[1]);
+    float best[kMaxVariants];
+    for (int j = 0; j < n; ++j) best[j] = 3.4e38f;
+    for (int pass = 0; pass < 2 && e == hipSuccess; ++pass)
+        for (int j = 0; j < n && e == hipSuccess; ++j) {
+            e = launch(j);
+            if (e == hipSuccess) e = hipEventRecord(ev[0], c->stream);
+            for (int r = 0; r < reps && e == hipSuccess; ++r) e = launch(j);
+            if (e == hipSuccess) e = hipEventRecord(ev[1], c->stream);
+            if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
+            float ms = 0.f;
+            if (e == hipSuccess && (e = hipEventElapsedTime(&ms, ev[0], ev[1])) == hipSuccess)
+                best[j] = std::min(best[j], ms);
+        }
+    if (e == hipSuccess) {
+        *win = 0;
+        for (int j = 1; j < n; ++j)
+            if (best[j] < best[*win]) *win = j;
+    }
+    for (hipEvent_t x : ev)
+        if (x) (void)hipEventDestroy(x);
+    return e;
+}
+
+// Whether the step + sync modes keep non-temporal accesses.  Beyond 1 GiB of
+// x and m they do (measured 10% faster at K = 8, P = 138M).  Between the
+// last-level cache's 256 MB and 1 GiB it depends on the problem (the fused
+// step + sync measured 14% faster without them at K = 32, P = 1.2M, and 14%
+// slower at K = 8, P = 11.2M), so time periods of four steps (three plain
+// steps, non-temporal as always, then the fused step + sync) with the sync's
+// accesses non-temporal and not.  The launches step x and m, which the caller
+// zeroes afterwards.
+constexpr double kSyncNtTuneMaxBytes = 1024.0 * 1024 * 1024;
+
+hipError_t tune_sync_nt(adpsgd_ctx *c) {
+    c->sync_nt = c->nontemporal;
+    if (!c->nontemporal || c->tiles.empty() || (double)c->K * (double)c->P * 8.0 > kSyncNtTuneMaxBytes)
+        return hipSuccess;
+    const StepParams stp = step_params(c, 0);
+    const SyncParams sp = sync_params(c, 3);
+    const int64_t n_tiles = (int64_t)c->tiles.size();
+    int win = 0;
+    const hipError_t e = fastest_in_blocks(
+        c, 2, 3,
+        [&](int j) {
+            hipError_t le = hipSuccess;
+            for (int i = 0; i < 3 && le == hipSuccess; ++i)
+                le = launch_local_step(stp, c->vec, c->nontemporal, c->step_shape, c->stream);
+            if (le == hipSuccess)
+                le = launch_tile_sync(sp, n_tiles, kFused, c->hp.avg_momentum != 0, c->vec, j == 0, 0, c->stream);
+            return le;
+        },
+        &win);
+    if (e == hipSuccess) c->sync_nt = win == 0;
+    return e;
+}
+
 // Time the separate sync (mean, broadcast and variance of every tile, no step)
 // without and with an LDS cap that holds a CU to kAverageCapWaves resident
-// waves, on the context's own buffers (zeroed again afterwards).
-hipError_t tune_average_cap(adpsgd_ctx *c) {
+// waves and, on x and m of 256 MB to 1 GiB (beyond the last-level cache, see
+// tune_sync_nt), with and without non-temporal accesses, on the context's own
+// buffers (zeroed again afterwards).
+hipError_t tune_average(adpsgd_ctx *c) {
     const int waves = sync_tile_waves(c->K, kAverage);
     if (waves <= 0 || c->tiles.empty()) return hipSuccess;
     const int caps[2] = {0, std::max(1, kAverageCapWaves / waves)};
+    const bool both = c->nontemporal && (double)c->K * (double)c->P * 8.0 <= kSyncNtTuneMaxBytes;
+    const int n = both ? 4 : 2;   // j: cap caps[j & 1], non-temporal while j < 2 (if at all)
     const SyncParams sp = sync_params(c, 0);
     const int64_t n_tiles = (int64_t)c->tiles.size();
     int win = 0;
-    const hipError_t e = fastest_variant(
-        c, 2,
+    const hipError_t e = fastest_in_blocks(
+        c, n, 3,
         [&](int j) {
-            return launch_tile_sync(sp, n_tiles, kAverage, c->hp.avg_momentum != 0, c->vec, c->nontemporal, caps[j],
-                                    c->stream);
+            return launch_tile_sync(sp, n_tiles, kAverage, c->hp.avg_momentum != 0, c->vec, c->nontemporal && j < 2,
+                                    caps[j & 1], c->stream);
         },
         &win);
-    if (e == hipSuccess) c->average_cap = caps[win];
+    if (e == hipSuccess) {
+        c->average_cap = caps[win & 1];
+        c->average_nt = c->nontemporal && win < 2;
+    }
     return e;
 }
 
@@ -691,6 +769,7 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
     c->vec = (c->ld % 4) == 0;
     // x and m beyond the 256 MB last-level cache: stream them past the caches
     c->nontemporal = (double)K * (double)P * 8.0 > 256.0 * 1024 * 1024;
+    c->sync_nt = c->average_nt = c->nontemporal;   // until timed
     c->rk = round_keys(hp->seed);
     char *ws = (char *)buf->workspace;
     c->d_tiles = (Tile *)(ws + lay.tiles);
@@ -763,7 +842,8 @@ extern "C" int adpsgd_init(int32_t K, int64_t P, const int64_t *offsets, int32_t
         if ((e = zero_rows(c)) != hipSuccess) return bail(e, "zero x and m");
         if ((double)K * (double)P >= kTuneMinElems) {
             if ((e = tune_step_shape(c)) != hipSuccess) return bail(e, "time the local step");
-            if ((e = tune_average_cap(c)) != hipSuccess) return bail(e, "time the separate sync");
+            if ((e = tune_sync_nt(c)) != hipSuccess) return bail(e, "time the fused step + sync");
+            if ((e = tune_average(c)) != hipSuccess) return bail(e, "time the separate sync");
             if ((e = zero_rows(c)) != hipSuccess) return bail(e, "zero x and m");
         }
     }
