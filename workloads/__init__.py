@@ -167,6 +167,15 @@ def full_workloads() -> dict:
     }
 
 
+def fullsize_variants() -> dict:
+    """Full-size variants used only by the tests: the 138M-parameter adaptive
+    workload with the step-decayed rate of the ResNet-shaped runs (x0.1 at steps
+    250 and 375), so that the controller moves p at that size (with the
+    constant rate it keeps p = 4)."""
+    w = _cfg_vgg16_like(True)
+    return {"vgg16_stepdecay": w.replace(name="k8_p138m_t32_stepdecay_adaptive", lr_kind=LR_STEP)}
+
+
 def reduced(w: Workload, P: int, T: Optional[int] = None, steps: Optional[int] = None,
             minimum: int = 1, multiple: int = 1, stream: int = 7) -> Workload:
     """A smaller copy of `w` for element-by-element parity against the oracle.
