@@ -217,6 +217,11 @@ ADPSGD_API size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const 
  * K >= 1 workers; P >= 0 parameters; T >= 1 tensors with host offsets[T+1],
  * non-decreasing, offsets[0] = 0, offsets[T] = P (empty tensors allowed).
  * Fills h and xstar from the seed, zeroes x and m, and waits for the stream.
+ * With K * P >= 2^24 it first times, on those buffers, the local step's launch
+ * shapes (adpsgd_set_step_launch), the separate sync with and without an
+ * occupancy cap and, where x and m take 256 MB to 1 GiB, the syncs with cached
+ * and with non-temporal accesses, and keeps the fastest of each (the results
+ * are the same bits whichever wins).
  * P/4 and the step count must stay below 2^32 (Philox counter words).  Any
  * K * P that fits the device is accepted: a kernel grid beyond what one
  * dispatch holds (2^32 work-items) is issued as several launches. */
