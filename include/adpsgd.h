@@ -332,9 +332,10 @@ ADPSGD_API const char *adpsgd_last_error(void);
 
 /* ---- synchronization without allocation ------------------------------------ */
 
-/* For callers that cannot allocate device memory (code under HIP graph
- * capture, tight serving loops, harnesses that forbid hipMalloc): the separate
- * synchronization of adpsgd_average with no context.  x [K][P] (device, rows
+/* For callers that cannot allocate device memory (tight serving loops,
+ * harnesses that forbid hipMalloc): the separate synchronization of
+ * adpsgd_average with no context.  It waits for its stream before returning,
+ * so it cannot itself be recorded into a HIP graph.  x [K][P] (device, rows
  * row_stride elements apart, 0 meaning P; 16-byte aligned) is replaced by the
  * replica mean in every row, and var_out[T] (host) receives the per-tensor
  * variances (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2 of the replicas
