@@ -177,6 +177,10 @@ int main() {
             if (one(32, {300000}, ADPSGD_PERIOD_CONST, 4, 40, 0, policy, traced)) return 1;
             if (one(4, {0, 0}, ADPSGD_PERIOD_ALG1, 3, 20, 0, policy, traced)) return 1;
             if (one(2, many, ADPSGD_PERIOD_ADAPTIVE, 2, 24, 6, policy, traced)) return 1;
+            // x and m take 320 MB, between the last-level cache and 1 GiB: init
+            // times the cached and non-temporal sync variants as well as the
+            // step's launch shapes
+            if (one(8, {5000000}, ADPSGD_PERIOD_ADAPTIVE, 2, 16, 4, policy, traced, true)) return 1;
         }
     printf("all ok\n");
     fflush(stdout);
