@@ -32,11 +32,37 @@ HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "local_step_k8_p138m_traffic.md")
 
 
+def code_tokens(text: str) -> str:
+    """C++ source with its comments removed and every run of whitespace made one
+    space: what the compiler sees, so that edits to comments leave it alone."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        if text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif text[i] in "\"'":
+            j = i + 1
+            while j < n and text[j] != text[i]:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        else:
+            out.append(text[i])
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def kernel_source_digest() -> str:
+    """sha256 (first 16 hex digits) of the device sources' code, comments and
+    whitespace left out: profiles taken on the same code stay valid."""
     h = hashlib.sha256()
     for name in ("kernels.hip", "rng.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2007_06134_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2007_06134_amd", "csrc", name), encoding="utf-8") as f:
+            h.update(code_tokens(f.read()).encode() + b"\0")
     return h.hexdigest()[:16]
 
 

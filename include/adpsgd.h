@@ -109,7 +109,7 @@ typedef struct {
     int64_t total_steps; /* N: the schedule's length (step decay / cosine), >= 1  */
     int32_t p_init;      /* initial (or constant) averaging period, >= 1          */
     int32_t p_max;       /* upper bound on p; 0 means INT32_MAX                   */
-    int64_t k_s;         /* syncs after steps t < k_s sample C2 (Alg. 2, l. 13)   */
+    int64_t k_s;         /* syncs after steps t < k_s sample C2 (Algorithm 2)     */
     double thr_lo;       /* p += 1 if S < thr_lo * gamma_t * C2 (paper: 0.7)      */
     double thr_hi;       /* p -= 1 if S > thr_hi * gamma_t * C2 (paper: 1.3)      */
     int64_t sync_warmup_steps; /* steps t < this sync after every step with no controller
@@ -159,8 +159,8 @@ typedef struct {
  * faster than rows an even number of kilobytes apart. */
 ADPSGD_API int64_t adpsgd_padded_row_stride(int64_t P);
 
-/* Controller state on the host (Algorithm 2, lines 1-3).  x and m are the
- * device part of the state and stay in the caller's buffers. */
+/* Controller state on the host (Algorithm 2's inputs and counters).  x and m
+ * are the device part of the state and stay in the caller's buffers. */
 typedef struct {
     int64_t t;       /* next step index                          */
     int64_t cnt;     /* steps since the last sync (Alg. 2 cnt)   */
@@ -213,7 +213,7 @@ typedef struct {
  * boundaries offsets[0..T] (host).  Returns 0 if the arguments are invalid. */
 ADPSGD_API size_t adpsgd_workspace_bytes(int32_t K, int64_t P, int32_t T, const int64_t *offsets);
 
-/* Create a context (Algorithm 2, lines 1-3, and w_{0,i} = w_0 = 0).
+/* Create a context (Algorithm 2's initial state, and w_{0,i} = w_0 = 0).
  * K >= 1 workers; P >= 0 parameters; T >= 1 tensors with host offsets[T+1],
  * non-decreasing, offsets[0] = 0, offsets[T] = P (empty tensors allowed).
  * Fills h and xstar from the seed, zeroes x and m, and waits for the stream.
@@ -232,14 +232,14 @@ ADPSGD_API int adpsgd_init(int32_t K, int64_t P, const int64_t *tensor_offsets, 
  * C2 = 0.  h and xstar are kept.  Asynchronous. */
 ADPSGD_API int adpsgd_reset(adpsgd_ctx *c);
 
-/* Enqueue n >= 0 plain local steps t .. t+n-1 on every worker (Algorithm 2,
- * lines 5-7): d = h (x - x*) + sigma z + wd x; m = mu m + d; x = x - gamma_t m.
+/* Enqueue n >= 0 plain local steps t .. t+n-1 on every worker (Algorithm 2's
+ * update): d = h (x - x*) + sigma z + wd x; m = mu m + d; x = x - gamma_t m.
  * Advances t and cnt by n; a constant period that switches at p_switch_step
  * (hparams) becomes p_after in the state once a step t >= p_switch_step is
  * taken, as in adpsgd_sched_step.  Asynchronous. */
 ADPSGD_API int adpsgd_local_steps(adpsgd_ctx *c, int32_t n);
 
-/* Synchronize now (Algorithm 2, lines 9-12): xbar = mean of the K replicas,
+/* Synchronize now (Algorithm 2's sync): xbar = mean of the K replicas,
  * var_out[tau] = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2 (host, [T],
  * fp64), every replica set to xbar, momentum untouched, cnt = 0.  Blocks until
  * var_out is valid. */
@@ -250,10 +250,10 @@ ADPSGD_API int adpsgd_average(adpsgd_ctx *c, double *var_out);
  * Blocks. */
 ADPSGD_API int adpsgd_step_average(adpsgd_ctx *c, double *var_out);
 
-/* Period controller (Algorithm 2, lines 13-19) for a sync after step t - 1 with
- * S = sum(var[0..T)), as adpsgd_sched_on_sync.  Sampling phase (t-1 < k_s):
- * C2 <- running mean of S / gamma; otherwise p + 1 if S < thr_lo gamma C2,
- * p - 1 if S > thr_hi gamma C2.  Constant mode and the warm-up prefix: no
+/* Period controller (Algorithm 2's sampling and period decision) for a sync
+ * after step t - 1 with S = sum(var[0..T)), as adpsgd_sched_on_sync.
+ * Sampling phase (t-1 < k_s): C2 <- running mean of S / gamma; otherwise
+ * p + 1 if S < thr_lo gamma C2, p - 1 if S > thr_hi gamma C2.  Constant mode and the warm-up prefix: no
  * change.  *next_period (may be NULL) receives p.  ENONFINITE if S is NaN or
  * infinite: the counter still restarts (the sync took place), while p, C2 and
  * nC2 are unchanged. */
@@ -376,16 +376,16 @@ ADPSGD_API double adpsgd_lr(const adpsgd_hparams *hp, int64_t t);
 /* Initial controller state: t = cnt = nC2 = 0, C2 = 0, p = p_init. */
 ADPSGD_API int adpsgd_sched_init(const adpsgd_hparams *hp, adpsgd_state *st);
 
-/* Begin step t = st->t (Algorithm 2, line 5, and the test of line 8): cnt += 1,
+/* Begin step t = st->t (Algorithm 2's counter and its sync test): cnt += 1,
  * the period in force is set (p_after from p_switch_step on, constant modes),
  * and *sync_due = 1 if a sync follows this step: always during the warm-up
  * prefix, t mod p == 0 in ADPSGD_PERIOD_ALG1, cnt >= p otherwise.  Advances
  * st->t.  EINVAL on a NULL pointer. */
 ADPSGD_API int adpsgd_sched_step(const adpsgd_hparams *hp, adpsgd_state *st, int32_t *sync_due);
 
-/* Apply Algorithm 2, lines 9 and 13-19, for a sync after step t with variance
- * S: cnt = 0; in adaptive mode after the warm-up prefix, C2 sampling (t < k_s)
- * or p +- 1.  *margin (may be NULL) receives the decision margin (NaN if no
+/* Apply Algorithm 2's counter restart, sampling and period decision for a sync
+ * after step t with variance S: cnt = 0; in adaptive mode after the warm-up
+ * prefix, C2 sampling (t < k_s) or p +- 1.  *margin (may be NULL) receives the decision margin (NaN if no
  * decision).  ENONFINITE if S is not finite: cnt = 0 as after every sync,
  * with p, C2 and nC2 unchanged; EINVAL on a NULL pointer. */
 ADPSGD_API int adpsgd_sched_on_sync(const adpsgd_hparams *hp, adpsgd_state *st, int64_t t, double S,

@@ -229,7 +229,7 @@ void orc_problem_data(const orc_problem *pb, const int64_t *idx, int64_t n, doub
     }
 }
 
-/* One local step t on every worker (Algorithm 2, lines 6-7, with heavy-ball
+/* One local step t on every worker (Algorithm 2's update, with heavy-ball
  * momentum as in PyTorch SGD: d = g + wd*x; v = mu*v + d; x = x - gamma*v).
  * x and v are [K][n] over the selected elements idx[0..n) (all if idx NULL). */
 void orc_local_step(const orc_problem *pb, const int64_t *idx, int64_t n, int64_t t,
@@ -275,7 +275,7 @@ static void tensor_range(const orc_problem *pb, const int64_t *idx, int64_t n, i
     *je = lo;
 }
 
-/* The synchronization step (Algorithm 2, lines 10-12):
+/* The synchronization step of Algorithm 2 (average, then broadcast):
  *   xbar_i  = (1/K) sum_k x_{k,i}
  *   var_tau = (1/K) sum_k sum_{i in tau} (xbar_i - x_{k,i})^2      (pre-average x)
  *   x_{k,i} = xbar_i for every k; momentum untouched unless avg_momentum, in
@@ -368,10 +368,10 @@ double orc_grad_norm2(const orc_problem *pb, int64_t n, const double *x, const d
     return acc;
 }
 
-/* Period controller after a sync at step t with variance S (Algorithm 2,
- * lines 13-19).  Inactive in the constant modes and during the warm-up prefix
+/* Period controller after a sync at step t with variance S (Algorithm 2's
+ * sampling and period decision).  Inactive in the constant modes and during the warm-up prefix
  * (there the run synchronizes every step and Algorithm 2 has not started).
- * The period stays within [1, p_max]: line 19 would reach 0, and the paper
+ * The period stays within [1, p_max]: the decrease could reach 0, and the paper
  * gives no upper bound, so one is an option (p_max = 0: none).
  * Returns 0, or -4 if S is not finite (state unchanged). */
 int orc_controller(const orc_problem *pb, orc_state *st, int64_t t, double S)
@@ -397,11 +397,11 @@ void orc_state_init(const orc_problem *pb, orc_state *st)
     st->p = pb->p_init;
 }
 
-/* Start of step t: count it (Algorithm 2, line 5), apply the two-phase
+/* Start of step t: count it (Algorithm 2's counter), apply the two-phase
  * constant period (Section III-A strategies, Section V-B), and say whether a
  * sync follows it: every step of the p = 1 warm-up prefix (Sections III-B,
  * IV-C); t mod p == 0 under Algorithm 1's test; cnt == p under Algorithm 2's
- * (line 8; written >= so a period that shrinks under the counter still ends). */
+ * (written >= so a period that shrinks under the counter still ends). */
 static int begin_step(const orc_problem *pb, orc_state *st, int64_t t)
 {
     st->cnt += 1;

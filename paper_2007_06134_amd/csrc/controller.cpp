@@ -1,7 +1,8 @@
 // Host parts of ADPSGD: the learning-rate schedules and the adaptive period
-// controller (Algorithm 2, lines 1-3 and 13-19).  No device call here, so the
-// controller runs and is tested without a GPU; its rules are the inline
-// functions of schedule.hpp, which the device reduction kernel also uses.
+// controller (Algorithm 2's initial state, sampling and period decision).  No
+// device call here, so the controller runs and is tested without a GPU; its
+// rules are the inline functions of schedule.hpp, which the device reduction
+// kernel also uses.
 #include <algorithm>
 #include <climits>
 #include <cmath>

@@ -1,10 +1,10 @@
 // gfx950 kernels of the ADPSGD hot path.
 //
-//   k_local_step   one local step of every worker (Algorithm 2, lines 5-7): a
+//   k_local_step   one local step of every worker (Algorithm 2's update): a
 //                  streaming pass over x and m with the noisy quadratic
 //                  gradient generated in registers.
-//   k_sync_lds     the synchronization (Algorithm 2, lines 10-12) on one tile
-//                  of one tensor: replica mean, per-element squared deviations
+//   k_sync_lds     the synchronization of Algorithm 2 on one aligned chunk
+//                  of 256 elements: replica mean, per-element squared deviations
 //                  (the parameter variance of Section II-B), broadcast of the
 //                  mean; optionally fused behind the period's last local step
 //                  so a sync costs no extra pass over HBM.
@@ -755,7 +755,8 @@ __global__ void __launch_bounds__(kFinishThreads) k_reduce_windows(ReduceParams 
 // out[T + tau] = gradient norm^2, and S and the norm total are block sums.
 // Otherwise k_reduce_windows has written out, and S and the norm total are
 // block sums of its window partials.  With a schedule, thread 0 then applies
-// Algorithm 2's lines 13-19 (the same apply_sync as the host controller) and
+// Algorithm 2's sampling and period decision (the same apply_sync as the host
+// controller) and
 // writes the new state.  out and the record header are the host's pinned
 // record slot, written directly; the header is written in every case.
 __global__ void __launch_bounds__(kFinishThreads) k_reduce_finish(ReduceParams r) {

@@ -180,7 +180,8 @@ struct ReduceParams {
 };
 
 // Segmented fixed-order sums of the tile partials (chunks, then tensors, then
-// over tensors) and, with a schedule, Algorithm 2's lines 13-19 on the result.
+// over tensors) and, with a schedule, Algorithm 2's period decision on the
+// result.
 // Windows of tensors (ReduceParams::win_begin) are cut by the host:
 int32_t reduce_windows(int32_t T, const int32_t *chunk_begin, std::vector<int32_t> *win_begin);
 hipError_t launch_reduce(const ReduceParams &r, hipStream_t st);

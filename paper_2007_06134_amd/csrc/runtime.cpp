@@ -918,7 +918,7 @@ extern "C" int adpsgd_schedule(adpsgd_ctx *c, const double *var, int32_t *next_p
 // any other step runs the sync-tile kernel in a device-decided mode, which
 // steps and, iff Algorithm 2's counter (read from the device copy of the
 // controller state) says so, averages, followed by the reduction kernel that
-// sums the variances and applies lines 13-19 on the device.  After a decisive
+// sums the variances and takes Algorithm 2's period decision on the device.  After a decisive
 // sync the host waits for its outcome only while the GPU has queued steps
 // behind it; otherwise the device decides the next steps itself, so the GPU
 // never idles on a host round trip.  Every record is read back in order,

@@ -21,7 +21,7 @@ struct SchedRule {
     int64_t k_s;             // syncs after steps t < k_s sample C2
     int64_t warmup;          // steps t < warmup sync every step, with no controller update
     int64_t p_switch_step;   // 0: the period never switches
-    double thr_lo, thr_hi;   // bands of lines 16-19
+    double thr_lo, thr_hi;   // the bands of Algorithm 2's period decision
 };
 
 // Controller state between steps, as in adpsgd_state: t is the next step, cnt
@@ -57,12 +57,13 @@ ADPSGD_HD bool sync_decisive(const SchedRule &r, int64_t t) {
     return r.period_mode == ADPSGD_PERIOD_ADAPTIVE && t >= r.k_s && t >= r.warmup;
 }
 
-// Lines 13-19 after the sync that followed step t, with S the summed variance
-// and gamma step t's rate: the counter restarts; in the sampling phase
-// (t < K_s) C2 becomes the running mean of S / gamma; afterwards p moves by one
-// when S leaves [thr_lo gamma C2, thr_hi gamma C2] (p within [1, p_max]).
-// The sync took place whatever S is, so the counter restarts (line 9) in
-// every case; a non-finite S then returns false with C2, nC2 and p untouched.
+// Algorithm 2's sampling and period decision after the sync that followed
+// step t, with S the summed variance and gamma step t's rate: the counter
+// restarts; in the sampling phase (t < K_s) C2 becomes the running mean of
+// S / gamma; afterwards p moves by one when S leaves
+// [thr_lo gamma C2, thr_hi gamma C2] (p within [1, p_max]).  The sync took
+// place whatever S is, so the counter restarts in every case; a non-finite S
+// then returns false with C2, nC2 and p untouched.
 // margin (may be null): signed relative distance of S to the nearer band edge.
 ADPSGD_HD bool apply_sync(const SchedRule &r, int64_t t, double gamma, double S, SchedState *st, double *margin) {
     if (margin) *margin = __builtin_nan("");

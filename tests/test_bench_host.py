@@ -47,3 +47,14 @@ def test_more_than_one_gpu_is_refused(bench, monkeypatch, capsys):
         bench.main()
     assert e.value.code == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_source_digest_ignores_comments_not_code(bench):
+    """The counter figures describe compiled kernels: comment and whitespace
+    edits leave the digest alone, a change of code does not."""
+    code = 'int f(int a) {  // the sum\n  /* twice */ return a + a; }\nconst char *s = "// kept";\n'
+    same = 'int f(int a) {\n  return a + a;   // another comment\n}\nconst char *s = "// kept";\n'
+    other = 'int f(int a) { return a * 2; }\nconst char *s = "// kept";\n'
+    assert bench.code_tokens(code) == bench.code_tokens(same)
+    assert bench.code_tokens(code) != bench.code_tokens(other)
+    assert '"// kept"' in bench.code_tokens(code)

@@ -5,7 +5,7 @@ The full-size GPU tests compare against these files, which the oracle wrote
 offline (make_fullsize_golden.py): an edit of the oracle's arithmetic would
 leave them comparing against stale numbers.  Each test recomputes the first
 sync of a stored run with the current oracle: its step, its S and every
-per-tensor variance (Algorithm 2, lines 5-11).  For the three 138M-parameter runs
+per-tensor variance (Algorithm 2's steps and sync).  For the three 138M-parameter runs
 (4.4e9 updates to their first sync) the oracle replays the 26 tensors of at
 most 1e6 elements: the first sync follows step p_init - 1 before any decision,
 so its schedule does not depend on the data and a subset replay is exact.

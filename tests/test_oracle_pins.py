@@ -191,7 +191,7 @@ def test_controller_huge_variance_clamps_period_at_one():
 
 
 def test_controller_period_cap():
-    """p stays within [1, p_max] (the reading of lines 16-19 with an upper bound):
+    """p stays within [1, p_max] (the reading of Algorithm 2's period decision with an upper bound):
     zero variance after sampling grows p by one per sync until the cap, then the
     period stays; a cap equal to p_init fixes the period; no cap grows on."""
     w = _adaptive()
