@@ -56,12 +56,18 @@ def code_tokens(text: str) -> str:
     return " ".join("".join(out).split())
 
 
+# Every source the profiled kernels are compiled from.
+KERNEL_SOURCES = ("paper_2007_06134_amd/csrc/kernels.hip", "paper_2007_06134_amd/csrc/rng.hpp",
+                  "paper_2007_06134_amd/csrc/kernels.hpp", "paper_2007_06134_amd/csrc/schedule.hpp",
+                  "include/adpsgd.h")
+
+
 def kernel_source_digest() -> str:
     """sha256 (first 16 hex digits) of the device sources' code, comments and
     whitespace left out: profiles taken on the same code stay valid."""
     h = hashlib.sha256()
-    for name in ("kernels.hip", "rng.hpp", "kernels.hpp"):
-        with open(os.path.join(ROOT, "paper_2007_06134_amd", "csrc", name), encoding="utf-8") as f:
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, name), encoding="utf-8") as f:
             h.update(code_tokens(f.read()).encode() + b"\0")
     return h.hexdigest()[:16]
 
